@@ -1,0 +1,602 @@
+"""Seeded synthetic suffix-restore workloads.
+
+This module is the one place where inputs are made, and both the CPU oracle
+(``oracle/``) and the GPU path (the ``libpkv`` binding) consume what it makes.
+It draws the random parts of a resume (per-block precision tags, the repair
+mask, page tables, the edit shift, key and value tensors) and encodes them
+into a checkpoint payload the way the offload side of PatchKV does
+(Section IV-D: gather block rows, compute per-block scales, pack FP16 / 8-bit /
+4-bit codes, cluster same-tag blocks into runs).
+
+It holds none of the restore's arithmetic: it never dequantizes, rotates or
+places a row.  The encoder it contains is the *inverse* direction (float ->
+codes), which the restore never performs.
+
+Checkpoint format written here (one request):
+
+* payload, per layer ``l`` in order, per tag in order FP16, K8V8, K8V4, K4V4,
+  per block ``b`` with that tag in ascending order (repair blocks included,
+  their bytes are poison): the block's K tile then its V tile.  A tile is the
+  block's ``B`` gathered cache rows, token-major ``[B][H][D]``, in the tag's
+  key (resp. value) format: FP16 = IEEE binary16, 8-bit = one u8 code per
+  channel, 4-bit = two codes per byte with channel ``2j`` in the low nibble of
+  byte ``j``.  Rows past the end of the suffix in the last block are padding
+  (code 0).
+* scales, fp16 ``[L][NB][H][2 (K, V)][2 (scale, zero)]``; a quantized channel
+  decodes as ``code * scale + zero``.  Entries of FP16 tiles and of repair
+  blocks are NaN.
+
+Value model (synthetic stand-in for the paper's long-context models, whose
+weights and QA datasets are not available here): stored keys and values are
+N(0, 1); a few rotary channel *pairs* ``(i, i + D/2)`` per (layer, head) are
+outliers scaled by 8.  Because the outlier scale is applied to both channels
+of a rotary pair, each pair stays an isotropic Gaussian, so a key rotated to
+any old position has the same distribution as the pre-rotation key and the
+stored (post-rotation) keys can be drawn directly.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+import os
+from concurrent.futures import ProcessPoolExecutor
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+TAG_FP16, TAG_K8V8, TAG_K8V4, TAG_K4V4 = 0, 1, 2, 3
+TAG_NAMES = ("FP16", "K8V8", "K8V4", "K4V4")
+KEY_BITS = (16, 8, 8, 4)
+VALUE_BITS = (16, 8, 4, 4)
+OUT_FP16, OUT_BF16 = 0, 1
+
+FP16_NAN_BITS = 0x7E00
+POISON_CODE = 0xFF
+
+# Seed streams (spawn keys) so every piece can be regenerated in isolation.
+_STREAM_TAGS, _STREAM_REPAIR, _STREAM_PAGES, _STREAM_POS, _STREAM_K, _STREAM_V = range(6)
+
+CONFIG_NAMES = ("tiny", "llama8b_1l", "llama8b_32l", "llama70b", "batched16")
+BASE_SEED = 26090
+
+
+@dataclasses.dataclass(frozen=True)
+class Shape:
+    """Model and cache geometry shared by every request of a restore."""
+
+    num_layers: int
+    num_kv_heads: int
+    head_dim: int
+    block_tokens: int
+    page_size: int
+    pool_pages: int
+    rope_theta: float
+    out_dtype: int  # OUT_FP16 or OUT_BF16
+
+    @property
+    def pool_slots(self) -> int:
+        return self.pool_pages * self.page_size
+
+    @property
+    def row_elems(self) -> int:
+        """Elements of one cache slot (all heads)."""
+        return self.num_kv_heads * self.head_dim
+
+    @property
+    def layer_elems(self) -> int:
+        return self.pool_slots * self.row_elems
+
+    @property
+    def cache_elems(self) -> int:
+        return self.num_layers * self.layer_elems
+
+
+@dataclasses.dataclass
+class Request:
+    """One resumed request: suffix geometry, edit shift, tags, repair mask, pages."""
+
+    suffix_tokens: int
+    delta: int
+    dst_row0: int
+    tags: np.ndarray  # uint8 [NB]
+    repair: np.ndarray  # uint8 [NB], nonzero = block in the repair set
+    page_table: np.ndarray  # int32 [num_logical_pages], -1 = unmapped
+    payload_offset: int = 0  # bytes
+    scale_offset: int = 0  # fp16 elements
+
+    @property
+    def num_blocks(self) -> int:
+        return len(self.tags)
+
+
+def num_blocks(n_tokens: int, block_tokens: int) -> int:
+    return -(-n_tokens // block_tokens)
+
+
+def tile_nbytes(bits: int, shape: Shape) -> int:
+    """Bytes of one K or V tile ([B][H][D]) stored with ``bits`` per channel."""
+    return shape.block_tokens * shape.num_kv_heads * shape.head_dim * bits // 8
+
+
+def encoded_layer_nbytes(shape: Shape, tags: np.ndarray) -> int:
+    counts = np.bincount(np.asarray(tags, dtype=np.int64), minlength=4)
+    return int(sum(int(counts[t]) * (tile_nbytes(KEY_BITS[t], shape) + tile_nbytes(VALUE_BITS[t], shape))
+                   for t in range(4)))
+
+
+def encoded_request_nbytes(shape: Shape, req: Request) -> Tuple[int, int]:
+    """(payload bytes, scale fp16 elements) of one request's checkpoint."""
+    return (shape.num_layers * encoded_layer_nbytes(shape, req.tags),
+            shape.num_layers * req.num_blocks * shape.num_kv_heads * 4)
+
+
+# ----------------------------------------------------------------------------
+# Encoder (offload direction: floats -> codes).  Not part of the restore.
+# ----------------------------------------------------------------------------
+
+def fp16_round_down(x: np.ndarray) -> np.ndarray:
+    """Largest binary16 value <= x (x finite, float64)."""
+    h = x.astype(np.float16)
+    too_big = h.astype(np.float64) > x
+    h[too_big] = np.nextafter(h[too_big], np.float16(-np.inf))
+    return h
+
+
+def fp16_round_up(x: np.ndarray) -> np.ndarray:
+    """Smallest binary16 value >= x (x finite, float64)."""
+    h = x.astype(np.float16)
+    too_small = h.astype(np.float64) < x
+    h[too_small] = np.nextafter(h[too_small], np.float16(np.inf))
+    return h
+
+
+def quantize_tiles(x: np.ndarray, n_valid: np.ndarray, bits: int):
+    """Asymmetric per-(block, head) quantizer.
+
+    ``x`` is float32 ``[nb, B, H, D]``; rows ``>= n_valid[i]`` of block ``i``
+    are padding and excluded from the range.  Zero = min rounded down to fp16,
+    scale = (max - zero) / (2^bits - 1) rounded up to fp16, code =
+    rint((x - zero) / scale) clipped to the code range (code 0 when the scale
+    is 0).  The rounding directions keep every element within half a step of
+    its decoded value.  Returns (codes uint8 [nb,B,H,D], scale fp16 [nb,H],
+    zero fp16 [nb,H]).
+    """
+    nb, B, H, D = x.shape
+    qmax = (1 << bits) - 1
+    valid = (np.arange(B)[None, :] < n_valid[:, None])  # [nb, B]
+    vmask = valid[:, :, None, None]
+    lo = np.where(vmask, x, np.float32(np.inf)).min(axis=(1, 3)).astype(np.float64)
+    hi = np.where(vmask, x, np.float32(-np.inf)).max(axis=(1, 3)).astype(np.float64)
+    zero = fp16_round_down(lo)
+    scale = fp16_round_up((hi - zero.astype(np.float64)) / qmax)
+    s64 = scale.astype(np.float64)[:, None, :, None]
+    z64 = zero.astype(np.float64)[:, None, :, None]
+    safe = np.where(s64 > 0, s64, 1.0)
+    q = np.rint((x.astype(np.float64) - z64) / safe)
+    q = np.where(s64 > 0, q, 0.0)
+    q = np.clip(q, 0, qmax)
+    q = np.where(vmask, q, 0.0)
+    return q.astype(np.uint8), scale, zero
+
+
+def pack_nibbles(codes: np.ndarray) -> np.ndarray:
+    """Two 4-bit codes per byte along the last axis; channel 2j -> low nibble."""
+    c = codes.reshape(codes.shape[:-1] + (codes.shape[-1] // 2, 2))
+    return (c[..., 0] | (c[..., 1] << 4)).astype(np.uint8)
+
+
+def _encode_tiles(x: np.ndarray, n_valid: np.ndarray, bits: int):
+    """Encode ``[nb, B, H, D]`` float32 tiles; returns (bytes [nb, tile_bytes], scale, zero)."""
+    nb = x.shape[0]
+    if bits == 16:
+        h = x.astype(np.float16)
+        pad = np.arange(x.shape[1])[None, :] >= n_valid[:, None]
+        h[pad] = np.float16(0)
+        nanf = np.full((nb, x.shape[2]), np.nan, dtype=np.float16)
+        return h.view(np.uint8).reshape(nb, -1), nanf, nanf
+    codes, s, z = quantize_tiles(x, n_valid, bits)
+    if bits == 4:
+        codes = pack_nibbles(codes)
+    return codes.reshape(nb, -1), s, z
+
+
+def draw_layer(shape: Shape, seed: int, req_index: int, layer: int, n_tokens: int,
+               outlier_pairs: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Stored (post-rotation) K and V of one layer: float32 ``[NB*B, H, D]``.
+
+    Rows ``>= n_tokens`` (padding of the last block) are zero.
+    """
+    B, H, D = shape.block_tokens, shape.num_kv_heads, shape.head_dim
+    rows = num_blocks(n_tokens, B) * B
+    rk = _rng(seed, _STREAM_K, req_index, layer)
+    rv = _rng(seed, _STREAM_V, req_index, layer)
+    k = rk.standard_normal((rows, H, D), dtype=np.float32)
+    v = rv.standard_normal((rows, H, D), dtype=np.float32)
+    if outlier_pairs > 0:
+        for h in range(H):
+            pairs = rk.choice(D // 2, size=outlier_pairs, replace=False)
+            ch = np.concatenate([pairs, pairs + D // 2])
+            k[:, h, ch] *= np.float32(8.0)
+    k[n_tokens:] = 0
+    v[n_tokens:] = 0
+    return k, v
+
+
+def encode_layer(shape: Shape, req: Request, k: np.ndarray, v: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Encode one layer of one request into (payload bytes, fp16 scale bits [NB, H, 2, 2])."""
+    B, H, D = shape.block_tokens, shape.num_kv_heads, shape.head_dim
+    NB = req.num_blocks
+    N = req.suffix_tokens
+    kt = k.reshape(NB, B, H, D)
+    vt = v.reshape(NB, B, H, D)
+    n_valid = np.minimum(B, N - np.arange(NB) * B).astype(np.int64)
+    scales = np.full((NB, H, 2, 2), np.nan, dtype=np.float16)
+    pieces: List[np.ndarray] = []
+    repair = np.asarray(req.repair) != 0
+    for tag in range(4):
+        blocks = np.nonzero(np.asarray(req.tags) == tag)[0]
+        if len(blocks) == 0:
+            continue
+        kb, ks, kz = _encode_tiles(kt[blocks], n_valid[blocks], KEY_BITS[tag])
+        vb, vs, vz = _encode_tiles(vt[blocks], n_valid[blocks], VALUE_BITS[tag])
+        rep = repair[blocks]
+        if rep.any():  # repair blocks are never read by a restore: poison them
+            poison_k = FP16_NAN_BITS if KEY_BITS[tag] == 16 else POISON_CODE
+            poison_v = FP16_NAN_BITS if VALUE_BITS[tag] == 16 else POISON_CODE
+            kb[rep] = _poison_bytes(kb.shape[1], poison_k, KEY_BITS[tag])
+            vb[rep] = _poison_bytes(vb.shape[1], poison_v, VALUE_BITS[tag])
+        if tag != TAG_FP16:
+            scales[blocks, :, 0, 0] = ks
+            scales[blocks, :, 0, 1] = kz
+            scales[blocks, :, 1, 0] = vs
+            scales[blocks, :, 1, 1] = vz
+        scales[blocks[rep]] = np.float16(np.nan)
+        pieces.append(np.concatenate([kb, vb], axis=1).reshape(-1))
+    payload = np.concatenate(pieces) if pieces else np.zeros(0, np.uint8)
+    return payload, scales.view(np.uint16)
+
+
+def _poison_bytes(nbytes: int, pattern: int, bits: int) -> np.ndarray:
+    if bits == 16:
+        return np.full(nbytes // 2, pattern, dtype=np.uint16).view(np.uint8)
+    return np.full(nbytes, pattern, dtype=np.uint8)
+
+
+def _rng(seed: int, *key: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(entropy=seed, spawn_key=tuple(key))))
+
+
+# ----------------------------------------------------------------------------
+# Pool pre-fill: a counter-based pattern so any region can be recomputed.
+# ----------------------------------------------------------------------------
+
+_PF_C1 = 0x45D9F3B  # < 2^31, so 32-bit x constant stays inside int64
+_PF_C2 = 0x2C1B3C6D
+
+
+def prefill_bits_np(flat_index: np.ndarray, seed: int) -> np.ndarray:
+    """uint16 pre-fill pattern of cache elements at the given flat indices."""
+    i = np.asarray(flat_index, dtype=np.int64)
+    x = ((i & 0xFFFFFFFF) ^ ((i >> 32) * 0x9E37) ^ (seed & 0xFFFF)) & 0xFFFFFFFF
+    x = ((x ^ (x >> 16)) * _PF_C1) & 0xFFFFFFFF
+    x = ((x ^ (x >> 15)) * _PF_C2) & 0xFFFFFFFF
+    x = x ^ (x >> 13)
+    return ((x >> 8) & 0xFFFF).astype(np.uint16)
+
+
+def prefill_bits_torch(flat_index, seed: int):
+    """Same pattern as :func:`prefill_bits_np` on an int64 torch tensor."""
+    i = flat_index
+    x = ((i & 0xFFFFFFFF) ^ ((i >> 32) * 0x9E37) ^ (seed & 0xFFFF)) & 0xFFFFFFFF
+    x = ((x ^ (x >> 16)) * _PF_C1) & 0xFFFFFFFF
+    x = ((x ^ (x >> 15)) * _PF_C2) & 0xFFFFFFFF
+    x = x ^ (x >> 13)
+    return (x >> 8) & 0xFFFF
+
+
+# ----------------------------------------------------------------------------
+# Cases
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class Case:
+    """A complete synthetic restore problem.
+
+    Layer ``l`` of request ``r`` is drawn with key ``(r, l % distinct_layers)``:
+    with ``distinct_layers < num_layers`` later layers repeat the encoded
+    bytes of earlier ones (still stored at their own addresses).
+    """
+
+    name: str
+    shape: Shape
+    requests: List[Request]
+    seed: int
+    distinct_layers: int
+    outlier_pairs: int
+    payload_nbytes: int = 0
+    scale_elems: int = 0
+    _layer_cache: Dict[Tuple[int, int], Tuple[np.ndarray, np.ndarray]] = dataclasses.field(
+        default_factory=dict, repr=False)
+
+    def __post_init__(self):
+        off, soff = 0, 0
+        for r in self.requests:
+            r.payload_offset = off
+            r.scale_offset = soff
+            pb, se = encoded_request_nbytes(self.shape, r)
+            off += _round_up(pb, 256)
+            soff += _round_up(se, 64)
+        self.payload_nbytes = off
+        self.scale_elems = soff
+
+    # -- raw draws and encoded layers ------------------------------------
+    def source_layer(self, layer: int) -> int:
+        return layer % self.distinct_layers
+
+    def raw_layer(self, req_index: int, layer: int) -> Tuple[np.ndarray, np.ndarray]:
+        r = self.requests[req_index]
+        return draw_layer(self.shape, self.seed, req_index, self.source_layer(layer), r.suffix_tokens,
+                          self.outlier_pairs)
+
+    def encoded_layer(self, req_index: int, layer: int) -> Tuple[np.ndarray, np.ndarray]:
+        key = (req_index, self.source_layer(layer))
+        if key not in self._layer_cache:
+            k, v = self.raw_layer(req_index, layer)
+            self._layer_cache[key] = encode_layer(self.shape, self.requests[req_index], k, v)
+        return self._layer_cache[key]
+
+    def warm(self, workers: Optional[int] = None) -> None:
+        """Encode every distinct (request, layer) once, in parallel processes."""
+        keys = [(ri, l) for ri in range(len(self.requests)) for l in range(min(self.distinct_layers,
+                                                                                self.shape.num_layers))]
+        keys = [k for k in keys if k not in self._layer_cache]
+        if not keys:
+            return
+        workers = workers or default_workers()
+        if workers <= 1 or len(keys) == 1:
+            for ri, l in keys:
+                self.encoded_layer(ri, l)
+            return
+        args = [(self.shape, self.requests[ri], self.seed, ri, l, self.outlier_pairs) for ri, l in keys]
+        with ProcessPoolExecutor(max_workers=min(workers, len(keys))) as ex:
+            for key, res in zip(keys, ex.map(_encode_job, args)):
+                self._layer_cache[key] = res
+
+    def layer_payload_offset(self, req_index: int, layer: int) -> int:
+        r = self.requests[req_index]
+        return r.payload_offset + layer * encoded_layer_nbytes(self.shape, r.tags)
+
+    def layer_scale_offset(self, req_index: int, layer: int) -> int:
+        r = self.requests[req_index]
+        return r.scale_offset + layer * r.num_blocks * self.shape.num_kv_heads * 4
+
+    def host_payload(self) -> Tuple[np.ndarray, np.ndarray]:
+        """Full (payload uint8, scales uint16) host arrays."""
+        payload = np.zeros(self.payload_nbytes, dtype=np.uint8)
+        scales = np.full(self.scale_elems, FP16_NAN_BITS, dtype=np.uint16)
+        for ri, r in enumerate(self.requests):
+            for l in range(self.shape.num_layers):
+                pb, sb = self.encoded_layer(ri, l)
+                o = self.layer_payload_offset(ri, l)
+                payload[o:o + pb.size] = pb
+                so = self.layer_scale_offset(ri, l)
+                scales[so:so + sb.size] = sb.reshape(-1)
+        return payload, scales
+
+    # -- pool ------------------------------------------------------------
+    def prefill_seed(self, which: int) -> int:
+        return (self.seed * 2 + which) & 0xFFFF
+
+    def host_prefill(self, which: int) -> np.ndarray:
+        """uint16 ``[L, pool_pages, P, H, D]`` pre-fill of the K (0) or V (1) cache."""
+        n = self.shape.cache_elems
+        bits = prefill_bits_np(np.arange(n, dtype=np.int64), self.prefill_seed(which))
+        s = self.shape
+        return bits.reshape(s.num_layers, s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim)
+
+    # -- accounting (data volume, not arithmetic) -------------------------
+    def restored_tokens(self) -> int:
+        """Tokens restored per layer summed over requests (rows of F blocks)."""
+        total = 0
+        B = self.shape.block_tokens
+        for r in self.requests:
+            n_valid = np.minimum(B, r.suffix_tokens - np.arange(r.num_blocks) * B)
+            total += int(n_valid[np.asarray(r.repair) == 0].sum())
+        return total
+
+    def algorithmic_bytes(self) -> Dict[str, int]:
+        """Bytes a restore must move: payload of F blocks, their scales, output rows."""
+        s = self.shape
+        B, H, D = s.block_tokens, s.num_kv_heads, s.head_dim
+        read = 0
+        scales = 0
+        for r in self.requests:
+            f = np.asarray(r.repair) == 0
+            n_valid = np.minimum(B, r.suffix_tokens - np.arange(r.num_blocks) * B)
+            for tag in range(4):
+                sel = f & (np.asarray(r.tags) == tag)
+                rows = int(n_valid[sel].sum())
+                read += rows * H * D * (KEY_BITS[tag] + VALUE_BITS[tag]) // 8
+                if tag != TAG_FP16:
+                    scales += int(sel.sum()) * H * 4 * 2
+        tok = self.restored_tokens()
+        written = tok * H * D * 2 * 2
+        L = s.num_layers
+        return {"payload_read": L * read, "scale_read": L * scales, "written": L * written,
+                "total": L * (read + scales + written)}
+
+
+def _encode_job(args):
+    shape, req, seed, ri, l, outlier_pairs = args
+    k, v = draw_layer(shape, seed, ri, l, req.suffix_tokens, outlier_pairs)
+    return encode_layer(shape, req, k, v)
+
+
+def default_workers() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def _round_up(x: int, a: int) -> int:
+    return (x + a - 1) // a * a
+
+
+# ----------------------------------------------------------------------------
+# Draws of tags, repair sets, positions and page tables
+# ----------------------------------------------------------------------------
+
+def draw_tags(rng: np.random.Generator, nb: int, mix: Sequence[float], int4_tag: int = TAG_K8V4) -> np.ndarray:
+    """Per-block tags from a (int4, int8, fp16) mix; int4 maps to K8V4 (or K4V4)."""
+    choices = np.array([int4_tag, TAG_K8V8, TAG_FP16], dtype=np.uint8)
+    p = np.asarray(mix, dtype=np.float64)
+    return choices[rng.choice(3, size=nb, p=p / p.sum())]
+
+
+def draw_repair_edit_local(rng: np.random.Generator, nb: int, frac: float, local_share: float = 0.8) -> np.ndarray:
+    """Repair mask: a contiguous run from block 0 (the edit-local dirty window)
+    holding ``local_share`` of the repaired blocks, plus sparse random blocks."""
+    n_rep = int(round(frac * nb))
+    n_local = min(n_rep, int(round(local_share * n_rep)))
+    mask = np.zeros(nb, dtype=np.uint8)
+    mask[:n_local] = 1
+    rest = np.arange(n_local, nb)
+    extra = rng.choice(rest, size=min(len(rest), n_rep - n_local), replace=False)
+    mask[extra] = 1
+    return mask
+
+
+def draw_positions(rng: np.random.Generator, delta: int, min_old: int = 1024, max_old: int = 8191) -> int:
+    """rho_0 = omega_0 + delta with omega_0 uniform so that rho_0 >= min_old."""
+    lo = max(0, -delta) + min_old
+    omega0 = int(rng.integers(lo, max(lo, max_old) + 1))
+    return omega0 + delta
+
+
+def private_page_table(rng: np.random.Generator, rows_end: int, page_size: int, pool_factor: int = 2):
+    """Map every logical page covering ``[0, rows_end)`` to a distinct random
+    page of a pool ``pool_factor`` times larger.  Returns (table, pool_pages)."""
+    nlp = -(-rows_end // page_size)
+    pool = pool_factor * nlp
+    return rng.choice(pool, size=nlp, replace=False).astype(np.int32), pool
+
+
+def make_case(name: str, seed: Optional[int] = None, distinct_layers: Optional[int] = None,
+              int4_tag: int = TAG_K8V4) -> Case:
+    """One of the five named workloads (see ``CONFIG_NAMES``)."""
+    idx = CONFIG_NAMES.index(name)
+    seed = BASE_SEED + idx if seed is None else seed
+    g = lambda stream: _rng(seed, stream)
+    if name == "tiny":
+        B, P, N = 16, 16, 512
+        nb = num_blocks(N, B)
+        tags = g(_STREAM_TAGS).integers(0, 3, size=nb).astype(np.uint8)
+        tags = np.array([int4_tag, TAG_K8V8, TAG_FP16], dtype=np.uint8)[tags]
+        repair = np.zeros(nb, np.uint8)
+        repair[g(_STREAM_REPAIR).choice(nb, size=4, replace=False)] = 1
+        pt = g(_STREAM_PAGES).permutation(64).astype(np.int32)
+        shape = Shape(1, 2, 64, B, P, 64, 10000.0, OUT_FP16)
+        req = Request(N, 37, 337, tags, repair, pt)
+        return Case(name, shape, [req], seed, distinct_layers or 1, outlier_pairs=0)
+    if name in ("llama8b_1l", "llama8b_32l", "llama70b"):
+        if name == "llama8b_1l":
+            L, B, P, N, out, theta = 1, 32, 16, 8192, OUT_FP16, 500000.0
+            mix, rep = (0.7, 0.2, 0.1), 0.10
+            delta = int(g(_STREAM_POS).integers(-2048, 2049))
+        elif name == "llama8b_32l":
+            L, B, P, N, out, theta = 32, 32, 16, 32768, OUT_BF16, 500000.0
+            mix, rep, delta = (0.7, 0.2, 0.1), 0.15, -1500
+        else:
+            L, B, P, N, out, theta = 80, 64, 32, 65536, OUT_BF16, 500000.0
+            mix, rep, delta = (0.6, 0.3, 0.1), 0.12, 4096
+        nb = num_blocks(N, B)
+        tags = draw_tags(g(_STREAM_TAGS), nb, mix, int4_tag)
+        repair = draw_repair_edit_local(g(_STREAM_REPAIR), nb, rep)
+        rho0 = draw_positions(g(_STREAM_POS) if name != "llama8b_1l" else _rng(seed, _STREAM_POS, 1), delta)
+        pt, pool = private_page_table(g(_STREAM_PAGES), rho0 + N, P)
+        shape = Shape(L, 8, 128, B, P, pool, theta, out)
+        req = Request(N, delta, rho0, tags, repair, pt)
+        return Case(name, shape, [req], seed, distinct_layers or L, outlier_pairs=1)
+    if name == "batched16":
+        return make_batched(seed, distinct_layers=distinct_layers or 2, int4_tag=int4_tag)
+    raise ValueError(name)
+
+
+def make_batched(seed: int, n_req: int = 16, num_layers: int = 32, pool_slots: int = 1 << 20,
+                 n_range: Tuple[int, int] = (4096, 65536), delta_range: Tuple[int, int] = (-8192, 8192),
+                 distinct_layers: int = 2, int4_tag: int = TAG_K8V4, B: int = 32, P: int = 16,
+                 H: int = 8, D: int = 128) -> Case:
+    """Batched resumes sharing one paged pool with interleaved page ownership."""
+    r_pos = _rng(seed, _STREAM_POS)
+    r_tags = _rng(seed, _STREAM_TAGS)
+    r_rep = _rng(seed, _STREAM_REPAIR)
+    r_pages = _rng(seed, _STREAM_PAGES)
+    pool_pages = pool_slots // P
+    reqs = []
+    spans = []
+    for _ in range(n_req):
+        N = int(r_pos.integers(n_range[0], n_range[1] + 1))
+        delta = int(r_pos.integers(delta_range[0], delta_range[1] + 1))
+        rho0 = draw_positions(r_pos, delta)
+        nb = num_blocks(N, B)
+        mix = r_tags.dirichlet((1.0, 1.0, 1.0))
+        tags = draw_tags(r_tags, nb, mix, int4_tag)
+        repair = draw_repair_edit_local(r_rep, nb, float(r_rep.uniform(0.05, 0.20)))
+        first, last = rho0 // P, (rho0 + N - 1) // P
+        spans.append((first, last))
+        reqs.append([N, delta, rho0, tags, repair])
+    need = sum(l - f + 1 for f, l in spans)
+    if need > pool_pages:
+        raise ValueError(f"batched case needs {need} pages, pool has {pool_pages}")
+    perm = r_pages.permutation(pool_pages).astype(np.int32)
+    tables = [np.full(l + 1, -1, dtype=np.int32) for f, l in spans]
+    cursor = [f for f, l in spans]
+    k = 0
+    live = True
+    while live:  # deal pool pages round-robin so ownership interleaves
+        live = False
+        for i, (f, l) in enumerate(spans):
+            if cursor[i] <= l:
+                tables[i][cursor[i]] = perm[k]
+                k += 1
+                cursor[i] += 1
+                live = True
+    shape = Shape(num_layers, H, D, B, P, pool_pages, 500000.0, OUT_BF16)
+    requests = [Request(N, d, r0, t, rp, tables[i]) for i, (N, d, r0, t, rp) in enumerate(reqs)]
+    return Case("batched16", shape, requests, seed, distinct_layers, outlier_pairs=1)
+
+
+def make_custom(seed: int, *, L: int = 1, H: int = 2, D: int = 64, B: int = 16, P: int = 16,
+                n_tokens: Sequence[int] = (100,), deltas: Sequence[int] = (5,), rho0s: Optional[Sequence[int]] = None,
+                mix: Sequence[float] = (1 / 3, 1 / 3, 1 / 3), tag_set: Sequence[int] = (TAG_K8V4, TAG_K8V8, TAG_FP16),
+                repair_frac: float = 0.2, repair_all: bool = False, out_dtype: int = OUT_FP16,
+                theta: float = 10000.0, outlier_pairs: int = 0, pool_factor: int = 2) -> Case:
+    """Small parametrised case for property tests (shared private pool, disjoint pages)."""
+    r = _rng(seed, 99)
+    reqs = []
+    ends = []
+    for i, N in enumerate(n_tokens):
+        delta = int(deltas[i % len(deltas)])
+        rho0 = int(rho0s[i]) if rho0s is not None else int(r.integers(0, 3 * P)) + max(0, 0)
+        nb = num_blocks(N, B)
+        p = np.asarray(mix, dtype=np.float64)
+        tags = np.asarray(tag_set, dtype=np.uint8)[r.choice(len(tag_set), size=nb, p=p / p.sum())]
+        if repair_all:
+            repair = np.ones(nb, np.uint8)
+        else:
+            repair = (r.random(nb) < repair_frac).astype(np.uint8)
+        reqs.append([N, delta, rho0, tags, repair])
+        ends.append(rho0 + N)
+    nlps = [max(1, -(-e // P)) for e in ends]
+    pool = pool_factor * sum(nlps)
+    perm = r.permutation(pool).astype(np.int32)
+    tables = []
+    k = 0
+    for n in nlps:
+        tables.append(perm[k:k + n].copy())
+        k += n
+    shape = Shape(L, H, D, B, P, pool, float(theta), out_dtype)
+    requests = [Request(N, d, r0, t, rp, tables[i]) for i, (N, d, r0, t, rp) in enumerate(reqs)]
+    return Case("custom", shape, requests, seed, L, outlier_pairs)

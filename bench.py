@@ -1,0 +1,255 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused suffix restore on one MI355X.
+
+One step = one ``pkv_restore`` of the whole workload (every layer, every
+reused block) from a device-resident checkpoint into device-resident paged
+caches.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload llama8b_32l] [--int4 K8V4|K4V4]
+
+Throughput is algorithmic bytes (payload and scales of reused blocks read,
+restored rows written) per second; the roofline entry divides the same bytes
+by the restore kernel's average duration from HIP events on its stream.
+The oracle, timed on the host cores on a bounded sample of the same
+workload, is reported beside it as ``cpu_baseline``.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import multiprocessing as mp
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "restored KV GB/s + % HBM peak; µs to restore 32K-token suffix (8B shape)"
+HBM_PEAK_GBPS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_26219_amd", "csrc", "restore.hip")
+
+WORKLOAD_TEXT = {
+    "llama8b_32l": "Llama-3-8B-shaped suffix restore: 32 layers x 8 KV heads x head_dim 128, 32768-token suffix, "
+                   "block 32, page 16, bf16 cache, tag mix 70% int4 / 20% int8 / 10% fp16, 15% repair blocks, "
+                   "delta -1500",
+    "llama8b_1l": "Llama-3-8B-shaped single layer: 8 KV heads x head_dim 128, 8192-token suffix, block 32, page 16, "
+                  "fp16 cache, 70/20/10 tag mix, 10% repair",
+    "llama70b": "Llama-70B-shaped: 80 layers x 8 KV heads x head_dim 128, 65536-token suffix, block 64, page 32, "
+                "bf16 cache, 60/30/10 tag mix, 12% repair, delta +4096",
+    "tiny": "tiny: 1 layer x 2 KV heads x head_dim 64, 512 tokens, block 16",
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str, int4: str):
+    """HBM bytes per launch from the committed rocprofv3 PMC summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"restore_kernel_{workload}_{int4.lower()}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"^traffic-json: (\{.*\})\s*$", open(path).read(), re.M)
+    if not m:
+        return None
+    d = json.loads(m.group(1))
+    if d.get("kernel_sha256_16") != kernel_hash():
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle, per layer, in worker processes
+# ---------------------------------------------------------------------------
+
+_CPU_CASE = None
+
+
+def _oracle_layer(args):
+    import dataclasses
+
+    import numpy as np
+
+    import oracle
+
+    ri, layer = args
+    case = _CPU_CASE
+    req = case.requests[ri]
+    pb, sb = case.encoded_layer(ri, layer)
+    one = dataclasses.replace(req, payload_offset=0, scale_offset=0)
+    s1 = dataclasses.replace(case.shape, num_layers=1)
+    cache = np.zeros((1, s1.pool_pages, s1.page_size, s1.num_kv_heads, s1.head_dim), np.uint16)
+    t = time.perf_counter()
+    oracle.restore(s1, [one], pb, sb.reshape(-1), cache, cache)
+    return time.perf_counter() - t
+
+
+def cpu_baseline(case, max_workers: int = 16, target_layers: int = 16):
+    """Oracle throughput on the host cores over a bounded sample of layers."""
+    global _CPU_CASE
+    _CPU_CASE = case
+    try:
+        n_cpu = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n_cpu = os.cpu_count() or 1
+    workers = max(1, min(max_workers, n_cpu))
+    layers = list(range(min(case.shape.num_layers, max(target_layers, workers))))
+    jobs = [(0, l) for l in layers]
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(workers) as pool:
+        per_layer = pool.map(_oracle_layer, jobs)
+    wall = time.perf_counter() - t0
+    per_layer_bytes = case.algorithmic_bytes()["total"] / case.shape.num_layers
+    sample_bytes = per_layer_bytes * len(layers)
+    return {
+        "value": round(sample_bytes / wall / 1e9, 4),
+        "unit": "GB/s",
+        "cores": workers,
+        "kind": "oracle",
+        "sample": f"{len(layers)} of {case.shape.num_layers} layers of the same workload (request 0), one process "
+                  f"per layer, {workers} processes; wall {wall:.1f} s, cpu {sum(per_layer):.1f} s",
+        "us_per_restore_extrapolated": round(wall / len(layers) * case.shape.num_layers * 1e6, 1),
+    }
+
+
+# ---------------------------------------------------------------------------
+
+
+def copy_reference(torch, nbytes: int = 4 << 30, reps: int = 10):
+    """Plain device-to-device copy (read + write bytes / time): the practical ceiling."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return round(2 * nbytes / (ms * 1e-3) / 1e9, 1)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b_32l", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--int4", default="K8V4", choices=["K8V4", "K4V4"],
+                    help="representation of the int4 tag: K8V4 (the paper's tier) or uniform K4V4")
+    ap.add_argument("--sets", type=int, default=2, help="buffer sets cycled between steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-copy-ref", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build restores on one GPU only; --gpus {args.gpus} is not supported "
+              f"(the restore shards by request, layer or KV head with no exchange step).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_26219_amd import binding
+    from paper_2609_26219_amd import workloads as wl
+    from paper_2609_26219_amd.device import DeviceRestore
+
+    binding.load()
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    int4_tag = wl.TAG_K8V4 if args.int4 == "K8V4" else wl.TAG_K4V4
+    t = time.perf_counter()
+    case = wl.make_case(args.workload, int4_tag=int4_tag)
+    case.warm()
+    log(f"[bench] generated {args.workload} in {time.perf_counter() - t:.1f} s")
+    sets = [DeviceRestore(case) for _ in range(max(1, args.sets))]
+    info = sets[0].info
+    nbytes = info["bytes_read"] + info["bytes_written"]
+    alg = case.algorithmic_bytes()
+    assert nbytes == alg["total"], (nbytes, alg)
+    log(f"[bench] {len(sets)} buffer set(s) ready; {info['num_units']} workgroups, {nbytes / 1e9:.3f} GB per step")
+
+    stream = torch.cuda.current_stream()
+    for i in range(args.warmup):
+        sets[i % len(sets)].run(stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        sets[i % len(sets)].run(stream)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = sorted(a.elapsed_time(b) for a, b in ev)
+    kern_avg_ms = sum(kern_ms) / len(kern_ms)
+    ms_per_step = wall * 1e3 / args.steps
+    log(f"[bench] kernel avg {kern_avg_ms * 1e3:.1f} us (median {kern_ms[len(kern_ms) // 2] * 1e3:.1f}), "
+        f"wall {ms_per_step * 1e3:.1f} us/step")
+
+    achieved = nbytes / (kern_avg_ms * 1e-3) / 1e9
+    value = nbytes / (ms_per_step * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32+f64",
+        "data": "synthetic",
+        "config": {
+            "workload": WORKLOAD_TEXT[args.workload],
+            "name": args.workload,
+            "int4_tag": args.int4,
+            "requests": len(case.requests),
+            "restored_tokens": case.restored_tokens(),
+            "algorithmic_bytes": nbytes,
+            "bytes_read": info["bytes_read"],
+            "bytes_written": info["bytes_written"],
+            "buffer_sets": len(sets),
+        },
+        "us_per_restore": round(kern_avg_ms * 1e3, 1),
+        "us_per_restore_p10_p50_p90": [round(kern_ms[int(q * (len(kern_ms) - 1))] * 1e3, 1) for q in (0.1, 0.5, 0.9)],
+        "pct_hbm_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
+        "restored_tokens_per_s": round(case.restored_tokens() / (kern_avg_ms * 1e-3), 1),
+        "output_GBps": round(info["bytes_written"] / (kern_avg_ms * 1e-3) / 1e9, 1),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": measured_traffic(args.workload, args.int4),
+        },
+    }
+    if not args.no_copy_ref:
+        del sets
+        torch.cuda.empty_cache()
+        out["copy_ref_GBps"] = copy_reference(torch)
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(case)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

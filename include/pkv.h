@@ -1,0 +1,184 @@
+/*
+ * pkv.h -- C ABI of libpkv: the fused suffix restore of PatchKV on MI355X.
+ *
+ * After a middle edit C_old = P + M_old + S  ->  C_new = P + M_new + S
+ * (PatchKV, Eq. 1), the blocks of the aligned suffix S that are not in the
+ * repair set R (Eq. 12) are restored from a quantized checkpoint: each block
+ * is decoded by its frozen precision tag (Eq. 14), its keys are re-phased by
+ * the edit shift Delta (Eq. 3; values are never rotated), and its rows are
+ * written into the request's destination KV pages (Section IV-D, the fused
+ * dequantize-and-scatter of the resume path, Section IV-A step 5).
+ *
+ * Usage: build an immutable plan once per resume (host validation, tile
+ * list, device metadata), launch it on a HIP stream as often as wanted, free
+ * it.  Every pointer in this header is a plain host or device address; no
+ * framework types appear.
+ *
+ * ----------------------------------------------------------------------------
+ * Checkpoint format (one request; all sizes follow from pkv_model_t and the
+ * request's tags -- pkv_payload_size() computes them):
+ *
+ *  payload (device, bytes): for each layer l = 0..L-1, for each tag in the
+ *    order FP16, K8V8, K8V4, K4V4, for each block b with that tag in
+ *    ascending order (repair blocks included; their bytes are never read):
+ *    the block's K tile, then its V tile.  A tile is the block's B rows in
+ *    token-major order [B][H][D] (rows past the end of the suffix in the last
+ *    block are padding).  Channel formats: FP16 = IEEE binary16; 8-bit = one
+ *    unsigned code per channel; 4-bit = two codes per byte, channel 2j in the
+ *    low nibble of byte j.  Same-tag blocks therefore form one contiguous run
+ *    per layer (the clustered runs of Section IV-D).
+ *
+ *  scales (device, binary16): [L][NB][H][2 (K, V)][2 (scale, zero)].  A
+ *    quantized channel decodes as code * scale + zero.  Entries of FP16
+ *    blocks are ignored.
+ *
+ *  caches (device): k_cache and v_cache, each [L][pool_pages][P][H][D] of the
+ *    output dtype (binary16 or bfloat16).  Token t of block b of a request
+ *    lands on logical row r = dst_row0 + b*B + t, physical slot
+ *    page_table[r / P] * P + r % P.  Nothing else is written: rows of repair
+ *    blocks, padding rows, prefix rows and pages owned by nobody keep their
+ *    bytes.
+ *
+ * Arithmetic: decode exact; keys rotated in double precision with a
+ * double-precision cos/sin(Delta * theta_i) table (theta_i =
+ * rope_theta^(-2i/D), rotate-half pairs (i, i + D/2)); values decoded in
+ * single precision; one round-to-nearest-even to the output dtype after an
+ * intermediate single-precision value.  Every element is within one unit in
+ * the last place of the exactly rounded result.  When Delta == 0 keys are
+ * not rotated at all (R(0) = I), so the FP16 tag with Delta == 0 and fp16
+ * output is a bit-exact copy.
+ * ----------------------------------------------------------------------------
+ */
+#ifndef PKV_H
+#define PKV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes.  Every entry point returns one; nothing is written to any
+ * device buffer when a call returns an error. */
+typedef enum {
+  PKV_OK = 0,
+  PKV_ERR_INVALID_ARGUMENT = -1,  /* null pointer, bad shape, misaligned buffer, buffer too small */
+  PKV_ERR_BAD_TAG = -2,           /* a block tag is not a pkv_tag_t value */
+  PKV_ERR_PAGE_OUT_OF_RANGE = -3, /* a written row's logical page is past the page table, or its
+                                     physical page is < -1 or >= pool_pages */
+  PKV_ERR_PAGE_UNMAPPED = -4,     /* a written row's logical page maps to -1 */
+  PKV_ERR_PAGE_ALIAS = -5,        /* one physical page written through two (request, logical page) pairs */
+  PKV_ERR_OUT_OF_MEMORY = -6,     /* host or device allocation failed */
+  PKV_ERR_DEVICE = -7             /* no usable GPU, wrong device, or a HIP call / launch failed */
+} pkv_status_t;
+
+/* Per-block precision tag (Eq. 14 tiers; K4V4 is the uniform 4-bit
+ * representation of the paper's transport ablation, Section V-C). */
+typedef enum {
+  PKV_TAG_FP16 = 0, /* keys and values binary16 */
+  PKV_TAG_K8V8 = 1, /* 8-bit keys, 8-bit values */
+  PKV_TAG_K8V4 = 2, /* 8-bit keys, 4-bit values */
+  PKV_TAG_K4V4 = 3  /* 4-bit keys, 4-bit values */
+} pkv_tag_t;
+
+typedef enum { PKV_OUT_FP16 = 0, PKV_OUT_BF16 = 1 } pkv_out_dtype_t;
+
+/* Model and cache geometry, shared by all requests of a plan.
+ * Constraints (else PKV_ERR_INVALID_ARGUMENT):
+ *   num_layers >= 1; 1 <= num_kv_heads; head_dim % 16 == 0, 16 <= head_dim <= 512;
+ *   num_kv_heads * head_dim <= 4096; 1 <= block_tokens <= 1024;
+ *   (block_tokens * num_kv_heads * head_dim) % 32 == 0 (every tile 16-byte aligned);
+ *   page_size a power of two in [1, 2^20]; pool_pages >= 1;
+ *   rope_theta finite and > 0; out_dtype a pkv_out_dtype_t value. */
+typedef struct {
+  int32_t num_layers;   /* L */
+  int32_t num_kv_heads; /* H */
+  int32_t head_dim;     /* D */
+  int32_t block_tokens; /* B: tokens per checkpoint block (the repair/reuse unit of Eq. 12) */
+  int32_t page_size;    /* P: token slots per KV page */
+  int32_t out_dtype;    /* pkv_out_dtype_t of k_cache / v_cache */
+  int64_t pool_pages;   /* pages per layer in each cache */
+  double rope_theta;    /* RoPE base */
+} pkv_model_t;
+
+/* One resumed request (one aligned suffix S).  Host arrays are copied by
+ * pkv_restore_plan; the caller may free them when it returns. */
+typedef struct {
+  int32_t suffix_tokens;       /* N = |S| >= 0; NB = ceil(N / B) blocks, the last may be partial */
+  int32_t delta;               /* Delta = rho_i - omega_i (new minus old position), the same for all of S */
+  int64_t dst_row0;            /* rho_0 >= 0: logical destination row of suffix token 0 */
+  const uint8_t* tags;         /* host [NB] pkv_tag_t (may be NULL when N == 0) */
+  const uint8_t* repair_mask;  /* host [NB], nonzero = block in R (skipped, its payload never read) */
+  const int32_t* page_table;   /* host [num_logical_pages], physical page or -1 = unmapped */
+  int32_t num_logical_pages;   /* >= 0 */
+  int32_t reserved;            /* must be 0 */
+  uint64_t payload_offset;     /* byte offset of this request's checkpoint in `payload`; % 16 == 0 */
+  uint64_t scale_offset;       /* binary16-element offset of its scales in `scales`; % 4 == 0 */
+} pkv_request_t;
+
+typedef struct pkv_plan pkv_plan_t; /* opaque, immutable once built */
+
+/* Sizes of one request's checkpoint: payload bytes and binary16 scale
+ * elements (layout above).  Host only, no GPU needed.  Validates the model
+ * and the tags. */
+pkv_status_t pkv_payload_size(const pkv_model_t* model, const pkv_request_t* request,
+                              uint64_t* payload_bytes, uint64_t* scale_elems);
+
+/* Validate a resume and build its plan on the current HIP device.
+ *   model, requests[0..num_requests) : as above (num_requests >= 0; 0 gives an empty plan);
+ *   out                              : receives the plan (set to NULL on error).
+ * All validation runs on the host before any HIP call (so every argument
+ * error is reported without a GPU): shapes, tags, reserved fields, offset
+ * alignment, every page touched by a row of a reused block (mapped, in
+ * range) and page ownership (no physical page written through two
+ * (request, logical page) pairs).  Then the tile list, per-request page
+ * tables and cos/sin(Delta * theta_i) tables (computed in double precision
+ * on the host) are copied to device memory owned by the plan (synchronous).
+ * Errors: any status above. */
+pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
+                              pkv_plan_t** out);
+
+/* Enqueue the restore described by `plan` on `hip_stream` (a hipStream_t;
+ * NULL = the default stream) and return without waiting.
+ *   payload      : device, >= the plan's payload_bytes (pkv_plan_query), 16-byte aligned;
+ *   scales       : device binary16, >= the plan's scale_bytes, 8-byte aligned;
+ *   k_cache/v_cache : device, each cache_bytes = L*pool_pages*P*H*D*2, 16-byte aligned,
+ *                  must not overlap each other or the inputs;
+ *   *_bytes      : the caller's allocation sizes, checked against what the plan reads / writes.
+ * The current device must be the plan's device.  All buffers must stay alive
+ * until the stream has passed the restore.  Calls that share a plan are safe
+ * concurrently only on disjoint caches.  Errors: PKV_ERR_INVALID_ARGUMENT,
+ * PKV_ERR_DEVICE (launch failure; asynchronous faults surface at the next
+ * synchronisation of the stream). */
+pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t payload_bytes, const void* scales,
+                         uint64_t scale_bytes, void* k_cache, void* v_cache, uint64_t cache_bytes, void* hip_stream);
+
+/* Release a plan and its device memory.  NULL is a no-op.  The caller must
+ * make sure no enqueued restore still uses it. */
+void pkv_free(pkv_plan_t* plan);
+
+/* What a plan reads and writes (for sizing buffers and for bandwidth
+ * accounting). */
+typedef struct {
+  int64_t num_requests;
+  int64_t num_units;          /* (request, layer, reused block) work units = workgroups launched */
+  int64_t restored_rows;      /* token rows written per cache, summed over layers and requests */
+  uint64_t payload_bytes;     /* bytes of `payload` the plan may touch (max over requests of offset + size) */
+  uint64_t scale_bytes;       /* bytes of `scales` likewise */
+  uint64_t cache_bytes;       /* bytes of each cache */
+  uint64_t bytes_read;        /* payload + scale bytes of reused blocks (what the restore must read) */
+  uint64_t bytes_written;     /* output bytes, K and V */
+  int32_t device;             /* HIP device the plan lives on */
+  int32_t reserved;
+} pkv_plan_info_t;
+
+pkv_status_t pkv_plan_query(const pkv_plan_t* plan, pkv_plan_info_t* info);
+
+/* Static description of a status code. */
+const char* pkv_status_string(pkv_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PKV_H */

@@ -109,11 +109,12 @@ def block_scales(scales: np.ndarray, req, shape, layer: int, block: int) -> np.n
     return bits.view(np.float16).astype(np.float64).reshape(H, 2, 2)
 
 
-def decode_block(payload: np.ndarray, scales: np.ndarray, shape, req, layer: int, block: int
-                 ) -> Tuple[np.ndarray, np.ndarray]:
-    """Decoded (K_old, V) of one block, fp64 ``[B, H, D]`` (padding rows included)."""
+def decode_block(payload: np.ndarray, scales: np.ndarray, shape, req, layer: int, block: int,
+                 layout: Optional[Tuple[Dict[int, Tuple[int, int]], int]] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Decoded (K_old, V) of one block, fp64 ``[B, H, D]`` (padding rows included).
+    ``layout`` is the request's ``block_layout`` if already computed."""
     B, H, D = shape.block_tokens, shape.num_kv_heads, shape.head_dim
-    offsets, layer_bytes = block_layout(req.tags, B, H, D)
+    offsets, layer_bytes = layout if layout is not None else block_layout(req.tags, B, H, D)
     base = req.payload_offset + layer * layer_bytes
     k_off, v_off = offsets[block]
     tag = int(req.tags[block])
@@ -222,11 +223,11 @@ def reused_blocks(req) -> List[int]:
     return [b for b in range(len(req.tags)) if int(req.repair[b]) == 0]
 
 
-def restore_block(payload, scales, shape, req, layer: int, block: int
+def restore_block(payload, scales, shape, req, layer: int, block: int, layout=None
                   ) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """(slots [n], K exact fp64 [n, H, D], V exact fp64 [n, H, D]) of one reused block."""
     n = valid_tokens(req, shape.block_tokens, block)
-    k_old, v = decode_block(payload, scales, shape, req, layer, block)
+    k_old, v = decode_block(payload, scales, shape, req, layer, block, layout)
     k = correct_key_phase(k_old[:n], int(req.delta), float(shape.rope_theta))
     return destination_slots(shape, req, block), k, v[:n]
 
@@ -244,9 +245,10 @@ def restore(shape, requests: Sequence, payload: np.ndarray, scales: np.ndarray,
     layer_list = range(L) if layers is None else list(layers)
     check_pages(shape, requests)
     for req in requests:
+        layout = block_layout(req.tags, shape.block_tokens, H, D)
         for layer in layer_list:
             for b in reused_blocks(req):
-                slots, k, v = restore_block(payload, scales, shape, req, layer, b)
+                slots, k, v = restore_block(payload, scales, shape, req, layer, b, layout)
                 kf[layer, slots] = round_to_output(k, shape.out_dtype)
                 vf[layer, slots] = round_to_output(v, shape.out_dtype)
     return k_out, v_out

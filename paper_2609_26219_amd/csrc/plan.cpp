@@ -1,0 +1,243 @@
+// Host half of libpkv: argument validation, the checkpoint layout, the work
+// list and the RoPE correction tables.  Pure C++ (no HIP calls), so every
+// validation path runs without a GPU.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+#include <limits>
+#include <new>
+#include <tuple>
+#include <vector>
+
+#include "pkv.h"
+#include "pkv_internal.h"
+
+namespace pkv {
+namespace {
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int ilog2(int64_t x) {
+  int r = 0;
+  while ((int64_t(1) << r) < x) ++r;
+  return r;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+pkv_status_t check_model(const pkv_model_t* m) {
+  if (!m) return PKV_ERR_INVALID_ARGUMENT;
+  if (m->num_layers < 1 || m->num_kv_heads < 1) return PKV_ERR_INVALID_ARGUMENT;
+  if (m->head_dim < 16 || m->head_dim > kMaxHeadDim || m->head_dim % 16 != 0) return PKV_ERR_INVALID_ARGUMENT;
+  if (int64_t(m->num_kv_heads) * m->head_dim > kMaxRowElems) return PKV_ERR_INVALID_ARGUMENT;
+  if (m->block_tokens < 1 || m->block_tokens > kMaxBlockTokens) return PKV_ERR_INVALID_ARGUMENT;
+  if ((int64_t(m->block_tokens) * m->num_kv_heads * m->head_dim) % 32 != 0) return PKV_ERR_INVALID_ARGUMENT;
+  if (!is_pow2(m->page_size) || m->page_size > (1 << 20)) return PKV_ERR_INVALID_ARGUMENT;
+  if (m->pool_pages < 1) return PKV_ERR_INVALID_ARGUMENT;
+  if (!(isfinite(m->rope_theta) && m->rope_theta > 0.0)) return PKV_ERR_INVALID_ARGUMENT;
+  if (m->out_dtype != PKV_OUT_FP16 && m->out_dtype != PKV_OUT_BF16) return PKV_ERR_INVALID_ARGUMENT;
+  // Cache elements per layer and in total must stay far from int64 overflow.
+  const double elems = double(m->num_layers) * double(m->pool_pages) * m->page_size * m->num_kv_heads * m->head_dim;
+  if (elems > 1e18) return PKV_ERR_INVALID_ARGUMENT;
+  return PKV_OK;
+}
+
+pkv_status_t check_request_fields(const pkv_request_t& r) {
+  if (r.reserved != 0) return PKV_ERR_INVALID_ARGUMENT;
+  if (r.suffix_tokens < 0 || r.num_logical_pages < 0 || r.dst_row0 < 0) return PKV_ERR_INVALID_ARGUMENT;
+  if (r.dst_row0 > (int64_t(1) << 50)) return PKV_ERR_INVALID_ARGUMENT;
+  if (r.suffix_tokens > 0 && (!r.tags || !r.repair_mask)) return PKV_ERR_INVALID_ARGUMENT;
+  if (r.num_logical_pages > 0 && !r.page_table) return PKV_ERR_INVALID_ARGUMENT;
+  if (r.payload_offset % 16 != 0 || r.scale_offset % 4 != 0) return PKV_ERR_INVALID_ARGUMENT;
+  if (r.payload_offset > (uint64_t(1) << 56) || r.scale_offset > (uint64_t(1) << 56)) return PKV_ERR_INVALID_ARGUMENT;
+  return PKV_OK;
+}
+
+pkv_status_t check_tags(const pkv_request_t& r, int64_t nb) {
+  for (int64_t b = 0; b < nb; ++b)
+    if (r.tags[b] > PKV_TAG_K4V4) return PKV_ERR_BAD_TAG;
+  return PKV_OK;
+}
+
+uint64_t tile_bytes(const pkv_model_t& m, int bits) {
+  return uint64_t(m.block_tokens) * m.num_kv_heads * m.head_dim * bits / 8;
+}
+
+}  // namespace
+
+uint64_t layer_payload_bytes(const pkv_model_t& m, const uint8_t* tags, int64_t nb) {
+  uint64_t total = 0;
+  for (int64_t b = 0; b < nb; ++b) total += tile_bytes(m, kKeyBits[tags[b]]) + tile_bytes(m, kValueBits[tags[b]]);
+  return total;
+}
+
+pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
+                             HostPlan* out) {
+  pkv_status_t st = check_model(model);
+  if (st != PKV_OK) return st;
+  if (num_requests < 0 || (num_requests > 0 && !requests) || !out) return PKV_ERR_INVALID_ARGUMENT;
+  const pkv_model_t& m = *model;
+  const int64_t B = m.block_tokens, H = m.num_kv_heads, D = m.head_dim, P = m.page_size, L = m.num_layers;
+  const int lp2 = ilog2(P);
+
+  // Field, tag and page checks, request by request.
+  for (int32_t r = 0; r < num_requests; ++r) {
+    const pkv_request_t& q = requests[r];
+    if ((st = check_request_fields(q)) != PKV_OK) return st;
+    const int64_t nb = ceil_div(q.suffix_tokens, B);
+    if ((st = check_tags(q, nb)) != PKV_OK) return st;
+  }
+  // Every page touched by a row of a reused block: in range and mapped;
+  // collect (physical page, request, logical page) for the ownership check.
+  std::vector<std::tuple<int64_t, int32_t, int64_t>> touched;
+  for (int32_t r = 0; r < num_requests; ++r) {
+    const pkv_request_t& q = requests[r];
+    const int64_t nb = ceil_div(q.suffix_tokens, B);
+    int64_t last_lp = -1;
+    for (int64_t b = 0; b < nb; ++b) {
+      if (q.repair_mask[b]) continue;
+      const int64_t n_valid = std::min<int64_t>(B, q.suffix_tokens - b * B);
+      const int64_t first_row = q.dst_row0 + b * B;
+      const int64_t last_row = first_row + n_valid - 1;
+      for (int64_t lp = std::max(first_row >> lp2, last_lp + 1); lp <= (last_row >> lp2); ++lp) {
+        if (lp >= q.num_logical_pages) return PKV_ERR_PAGE_OUT_OF_RANGE;
+        const int32_t pp = q.page_table[lp];
+        if (pp == -1) return PKV_ERR_PAGE_UNMAPPED;
+        if (pp < -1 || pp >= m.pool_pages) return PKV_ERR_PAGE_OUT_OF_RANGE;
+        touched.emplace_back(pp, r, lp);
+        last_lp = lp;
+      }
+    }
+  }
+  std::sort(touched.begin(), touched.end());
+  for (size_t i = 1; i < touched.size(); ++i) {
+    if (std::get<0>(touched[i]) == std::get<0>(touched[i - 1]) &&
+        (std::get<1>(touched[i]) != std::get<1>(touched[i - 1]) ||
+         std::get<2>(touched[i]) != std::get<2>(touched[i - 1])))
+      return PKV_ERR_PAGE_ALIAS;
+  }
+
+  // Build: tile list, per-request metadata, page tables, cos/sin tables.
+  HostPlan& hp = *out;
+  hp.model = m;
+  hp.log2_page = lp2;
+  hp.units.clear();
+  hp.reqs.clear();
+  hp.tables.clear();
+  hp.page_tables.clear();
+  memset(&hp.info, 0, sizeof(hp.info));
+  hp.info.num_requests = num_requests;
+  hp.info.cache_bytes = uint64_t(L) * uint64_t(m.pool_pages) * uint64_t(P) * uint64_t(H) * uint64_t(D) * 2;
+
+  try {
+    hp.reqs.resize(num_requests);
+    hp.tables.resize(size_t(num_requests) * size_t(D));
+    for (int32_t r = 0; r < num_requests; ++r) {
+      const pkv_request_t& q = requests[r];
+      const int64_t nb = ceil_div(q.suffix_tokens, B);
+      ReqDev& rd = hp.reqs[r];
+      rd.table_off = int64_t(r) * D;
+      rd.pt_off = int64_t(hp.page_tables.size());
+      rd.rotate = q.delta != 0;
+      rd.num_logical_pages = q.num_logical_pages;
+      rd.reserved = 0;
+      hp.page_tables.insert(hp.page_tables.end(), q.page_table, q.page_table + q.num_logical_pages);
+      // cos / sin of Delta * theta^(-2i/D), in double precision.
+      for (int64_t i = 0; i < D / 2; ++i) {
+        const double ang = double(q.delta) * pow(m.rope_theta, -2.0 * double(i) / double(D));
+        hp.tables[size_t(r) * D + 2 * i] = q.delta ? cos(ang) : 1.0;
+        hp.tables[size_t(r) * D + 2 * i + 1] = q.delta ? sin(ang) : 0.0;
+      }
+      if (nb == 0) continue;
+      // Block offsets inside one layer: runs by tag, ascending blocks.
+      std::vector<uint64_t> block_off(nb);
+      uint64_t pos = 0;
+      for (int tag = 0; tag < 4; ++tag)
+        for (int64_t b = 0; b < nb; ++b)
+          if (q.tags[b] == tag) {
+            block_off[b] = pos;
+            pos += tile_bytes(m, kKeyBits[tag]) + tile_bytes(m, kValueBits[tag]);
+          }
+      const uint64_t layer_bytes = pos;
+      hp.info.payload_bytes = std::max<uint64_t>(hp.info.payload_bytes, q.payload_offset + uint64_t(L) * layer_bytes);
+      hp.info.scale_bytes =
+          std::max<uint64_t>(hp.info.scale_bytes, (q.scale_offset + uint64_t(L) * nb * H * 4) * 2);
+      for (int64_t l = 0; l < L; ++l) {
+        for (int64_t b = 0; b < nb; ++b) {
+          if (q.repair_mask[b]) continue;
+          const int tag = q.tags[b];
+          const int64_t n_valid = std::min<int64_t>(B, q.suffix_tokens - b * B);
+          Unit u;
+          u.k_off = q.payload_offset + uint64_t(l) * layer_bytes + block_off[b];
+          u.v_off = u.k_off + tile_bytes(m, kKeyBits[tag]);
+          u.scale_off = q.scale_offset + (uint64_t(l) * nb + b) * H * 4;
+          u.row0 = q.dst_row0 + b * B;
+          u.layer = int32_t(l);
+          u.req = r;
+          u.tag = tag;
+          u.n_valid = int32_t(n_valid);
+          hp.units.push_back(u);
+          hp.info.restored_rows += n_valid;
+          hp.info.bytes_read += uint64_t(n_valid) * H * D * (kKeyBits[tag] + kValueBits[tag]) / 8;
+          if (tag != PKV_TAG_FP16) hp.info.bytes_read += uint64_t(H) * 4 * 2;
+        }
+      }
+    }
+  } catch (const std::bad_alloc&) {
+    return PKV_ERR_OUT_OF_MEMORY;
+  }
+  if (hp.units.size() > size_t(std::numeric_limits<int32_t>::max())) return PKV_ERR_INVALID_ARGUMENT;
+  hp.info.num_units = int64_t(hp.units.size());
+  hp.info.bytes_written = uint64_t(hp.info.restored_rows) * H * D * 2 * 2;
+  return PKV_OK;
+}
+
+}  // namespace pkv
+
+extern "C" {
+
+pkv_status_t pkv_payload_size(const pkv_model_t* model, const pkv_request_t* request, uint64_t* payload_bytes,
+                              uint64_t* scale_elems) {
+  pkv_status_t st = pkv::check_model(model);
+  if (st != PKV_OK) return st;
+  if (!request || !payload_bytes || !scale_elems) return PKV_ERR_INVALID_ARGUMENT;
+  if (request->suffix_tokens < 0) return PKV_ERR_INVALID_ARGUMENT;
+  const int64_t nb = pkv::ceil_div(request->suffix_tokens, model->block_tokens);
+  if (nb > 0 && !request->tags) return PKV_ERR_INVALID_ARGUMENT;
+  if ((st = pkv::check_tags(*request, nb)) != PKV_OK) return st;
+  *payload_bytes = uint64_t(model->num_layers) * pkv::layer_payload_bytes(*model, request->tags, nb);
+  *scale_elems = uint64_t(model->num_layers) * uint64_t(nb) * model->num_kv_heads * 4;
+  return PKV_OK;
+}
+
+// Internal test hook (not part of pkv.h): the host-built work list, so tests
+// can check every address the kernel derives from it without a GPU.
+pkv_status_t pkv_internal_host_units(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
+                                     void* units_out, int64_t capacity, int64_t* count) {
+  if (!count) return PKV_ERR_INVALID_ARGUMENT;
+  pkv::HostPlan hp;
+  pkv_status_t st = pkv::build_host_plan(model, requests, num_requests, &hp);
+  if (st != PKV_OK) return st;
+  *count = int64_t(hp.units.size());
+  if (units_out && capacity >= *count && *count > 0)
+    memcpy(units_out, hp.units.data(), hp.units.size() * sizeof(pkv::Unit));
+  return PKV_OK;
+}
+
+const char* pkv_status_string(pkv_status_t s) {
+  switch (s) {
+    case PKV_OK: return "ok";
+    case PKV_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case PKV_ERR_BAD_TAG: return "bad precision tag";
+    case PKV_ERR_PAGE_OUT_OF_RANGE: return "page out of range";
+    case PKV_ERR_PAGE_UNMAPPED: return "page unmapped";
+    case PKV_ERR_PAGE_ALIAS: return "physical page written through two logical pages";
+    case PKV_ERR_OUT_OF_MEMORY: return "out of memory";
+    case PKV_ERR_DEVICE: return "device error";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,389 @@
+// Device half of libpkv: the fused dequantize / RoPE-correct / scatter kernel
+// of the suffix restore (PatchKV Section IV-D, Eq. 3, Eq. 14) for gfx950,
+// and the C entry points that own device memory and launch it.
+//
+// Work decomposition.  One workgroup restores one unit = (request, layer,
+// reused block), all heads.  Its B rows are contiguous in the payload
+// (token-major tiles) and each row lands on one cache slot whose H*D
+// elements are contiguous, so a unit is a streaming row-to-row transform.
+// A thread owns a fixed "piece" of every row it touches: for keys, channels
+// [8j, 8j+8) and their rotary partners [D/2+8j, D/2+8j+8) of one head, so
+// the pair rotation needs no cross-lane exchange; for values, channels
+// [16j, 16j+16) of the same head.  Threads (t0, c) with c = head*(D/16)+j
+// walk tokens t0, t0+tpp, ... where tpp = 256 / (H*D/16).
+//
+// Arithmetic.  Codes decode exactly.  Keys are rotated in double precision
+// (full-rate on CDNA4) from a double (cos, sin) table staged in LDS, so the
+// rotated value carries ~2^-53 relative error even under cancellation;
+// values use one single-precision FMA.  Results go to float then to the
+// cache dtype with the hardware round-to-nearest-even conversions.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <new>
+
+#include "pkv.h"
+#include "pkv_internal.h"
+
+namespace pkv {
+namespace {
+
+constexpr int kMinWavesPerEU = 8;
+
+struct KernelArgs {
+  const Unit* units;
+  const ReqDev* reqs;
+  const double* tables;
+  const int32_t* page_tables;
+  const uint8_t* payload;
+  const uint16_t* scales;
+  uint16_t* k_cache;
+  uint16_t* v_cache;
+  int64_t layer_elems;  // pool_pages * P * H * D
+  int32_t H, D, log2P, cols, tpp;
+};
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h)));
+}
+
+// double -> float with the hardware conversion.  The empty asm pins the
+// float: without it the compiler merges double -> float -> half/bf16 into one
+// software double -> half/bf16 rounding of 10-40 integer instructions.
+__device__ __forceinline__ float to_float(double d) {
+  float f = static_cast<float>(d);
+  asm volatile("" : "+v"(f));
+  return f;
+}
+
+template <bool BF16>
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  if constexpr (BF16) {
+    const uint16_t x = __builtin_bit_cast(uint16_t, static_cast<__bf16>(a));
+    const uint16_t y = __builtin_bit_cast(uint16_t, static_cast<__bf16>(b));
+    return uint32_t(x) | (uint32_t(y) << 16);
+  } else {
+    const uint16_t x = __builtin_bit_cast(uint16_t, static_cast<_Float16>(a));
+    const uint16_t y = __builtin_bit_cast(uint16_t, static_cast<_Float16>(b));
+    return uint32_t(x) | (uint32_t(y) << 16);
+  }
+}
+
+template <bool BF16>
+__device__ __forceinline__ uint4 pack8(const float* v) {
+  return make_uint4(pack2<BF16>(v[0], v[1]), pack2<BF16>(v[2], v[3]), pack2<BF16>(v[4], v[5]),
+                    pack2<BF16>(v[6], v[7]));
+}
+
+// Eight channel codes / values of one half-row piece, as integers (codes) or
+// binary16 bit patterns (FP16 tag).
+template <int BITS>
+struct Chunk8;
+template <>
+struct Chunk8<16> {
+  uint4 w;
+  __device__ __forceinline__ void load(const uint8_t* p) { w = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ uint32_t raw(int e) const {
+    const uint32_t word = e < 2 ? w.x : e < 4 ? w.y : e < 6 ? w.z : w.w;
+    return (word >> (16 * (e & 1))) & 0xFFFFu;
+  }
+};
+template <>
+struct Chunk8<8> {
+  uint2 w;
+  __device__ __forceinline__ void load(const uint8_t* p) { w = *reinterpret_cast<const uint2*>(p); }
+  __device__ __forceinline__ uint32_t raw(int e) const { return ((e < 4 ? w.x : w.y) >> (8 * (e & 3))) & 0xFFu; }
+};
+template <>
+struct Chunk8<4> {
+  uint32_t w;
+  __device__ __forceinline__ void load(const uint8_t* p) { w = *reinterpret_cast<const uint32_t*>(p); }
+  __device__ __forceinline__ uint32_t raw(int e) const { return (w >> (4 * e)) & 0xFu; }
+};
+
+// Decode element e of a chunk to float (exact for codes <= 255 and binary16).
+template <int BITS>
+__device__ __forceinline__ float decode_f(const Chunk8<BITS>& c, int e, float s, float z) {
+  if constexpr (BITS == 16) {
+    return half_bits_to_float(c.raw(e));
+  } else {
+    return __builtin_fmaf(static_cast<float>(c.raw(e)), s, z);
+  }
+}
+
+template <int BITS>
+__device__ __forceinline__ double decode_d(const Chunk8<BITS>& c, int e, double s, double z) {
+  if constexpr (BITS == 16) {
+    return static_cast<double>(half_bits_to_float(c.raw(e)));
+  } else {
+    return __builtin_fma(static_cast<double>(c.raw(e)), s, z);
+  }
+}
+
+// Keys of one (token, head): piece j = channels [8j, 8j+8) and [D/2+8j, ...).
+template <int KBITS, bool ROT, bool BF16>
+__device__ __forceinline__ void restore_key_piece(const uint8_t* __restrict__ row, int j, int D, float ks, float kz,
+                                                  const double* __restrict__ tab, uint16_t* __restrict__ dst) {
+  Chunk8<KBITS> lo, hi;
+  lo.load(row + (8 * j) * KBITS / 8);
+  hi.load(row + (D / 2 + 8 * j) * KBITS / 8);
+  uint4 out_lo, out_hi;
+  if constexpr (KBITS == 16 && !ROT && !BF16) {
+    // binary16 in, binary16 out, no rotation: the bits are the result.
+    out_lo = lo.w;
+    out_hi = hi.w;
+  } else {
+    float a[8], b[8];
+    if constexpr (ROT) {
+      const double s64 = ks, z64 = kz;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const double x = decode_d<KBITS>(lo, e, s64, z64);
+        const double y = decode_d<KBITS>(hi, e, s64, z64);
+        const double2 cs = *reinterpret_cast<const double2*>(tab + 2 * (8 * j + e));
+        a[e] = to_float(__builtin_fma(x, cs.x, -(y * cs.y)));
+        b[e] = to_float(__builtin_fma(y, cs.x, x * cs.y));
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        a[e] = decode_f<KBITS>(lo, e, ks, kz);
+        b[e] = decode_f<KBITS>(hi, e, ks, kz);
+      }
+    }
+    out_lo = pack8<BF16>(a);
+    out_hi = pack8<BF16>(b);
+  }
+  *reinterpret_cast<uint4*>(dst + 8 * j) = out_lo;
+  *reinterpret_cast<uint4*>(dst + D / 2 + 8 * j) = out_hi;
+}
+
+// Values of one (token, head): piece j = channels [16j, 16j+16); never rotated.
+template <int VBITS, bool BF16>
+__device__ __forceinline__ void restore_value_piece(const uint8_t* __restrict__ row, int j, float vs, float vz,
+                                                    uint16_t* __restrict__ dst) {
+  Chunk8<VBITS> c0, c1;
+  c0.load(row + (16 * j) * VBITS / 8);
+  c1.load(row + (16 * j + 8) * VBITS / 8);
+  uint4 o0, o1;
+  if constexpr (VBITS == 16 && !BF16) {
+    o0 = c0.w;
+    o1 = c1.w;
+  } else {
+    float a[8], b[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      a[e] = decode_f<VBITS>(c0, e, vs, vz);
+      b[e] = decode_f<VBITS>(c1, e, vs, vz);
+    }
+    o0 = pack8<BF16>(a);
+    o1 = pack8<BF16>(b);
+  }
+  *reinterpret_cast<uint4*>(dst + 16 * j) = o0;
+  *reinterpret_cast<uint4*>(dst + 16 * j + 8) = o1;
+}
+
+template <int TAG, bool ROT, bool BF16>
+__device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u, const double* __restrict__ s_tab,
+                                             const int64_t* __restrict__ s_slot, int t0, int head, int j) {
+  constexpr int KB = kKeyBits[TAG];
+  constexpr int VB = kValueBits[TAG];
+  const int H = a.H, D = a.D;
+  float ks = 0.f, kz = 0.f, vs = 0.f, vz = 0.f;
+  if constexpr (TAG != PKV_TAG_FP16) {
+    const uint2 sw = *reinterpret_cast<const uint2*>(a.scales + u.scale_off + 4 * head);
+    ks = half_bits_to_float(sw.x & 0xFFFFu);
+    kz = half_bits_to_float(sw.x >> 16);
+    vs = half_bits_to_float(sw.y & 0xFFFFu);
+    vz = half_bits_to_float(sw.y >> 16);
+  }
+  const uint8_t* kbase = a.payload + u.k_off;
+  const uint8_t* vbase = a.payload + u.v_off;
+  const int64_t krow_bytes = int64_t(D) * KB / 8, vrow_bytes = int64_t(D) * VB / 8;
+  for (int t = t0; t < u.n_valid; t += a.tpp) {
+    const int64_t r = int64_t(t) * H + head;
+    const int64_t dst = s_slot[t] + int64_t(head) * D;
+    restore_key_piece<KB, ROT, BF16>(kbase + r * krow_bytes, j, D, ks, kz, s_tab, a.k_cache + dst);
+    restore_value_piece<VB, BF16>(vbase + r * vrow_bytes, j, vs, vz, a.v_cache + dst);
+  }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(KernelArgs a) {
+  __shared__ __attribute__((aligned(16))) double s_tab[kMaxHeadDim];
+  __shared__ int64_t s_slot[kMaxBlockTokens];
+  const Unit u = a.units[blockIdx.x];
+  const ReqDev rq = a.reqs[u.req];
+  const int tid = threadIdx.x;
+  if (rq.rotate)
+    for (int i = tid; i < a.D; i += kWorkgroup) s_tab[i] = a.tables[rq.table_off + i];
+  const int64_t P = int64_t(1) << a.log2P;
+  for (int t = tid; t < u.n_valid; t += kWorkgroup) {
+    const int64_t row = u.row0 + t;
+    const int64_t page = a.page_tables[rq.pt_off + (row >> a.log2P)];
+    s_slot[t] = int64_t(u.layer) * a.layer_elems + (page * P + (row & (P - 1))) * int64_t(a.H) * a.D;
+  }
+  __syncthreads();
+  const int t0 = tid / a.cols;
+  if (t0 >= a.tpp) return;
+  const int c = tid - t0 * a.cols;
+  const int dq = a.D >> 4;
+  const int head = c / dq;
+  const int j = c - head * dq;
+  switch (u.tag * 2 + (rq.rotate ? 1 : 0)) {
+    case 0: restore_unit<PKV_TAG_FP16, false, BF16>(a, u, s_tab, s_slot, t0, head, j); break;
+    case 1: restore_unit<PKV_TAG_FP16, true, BF16>(a, u, s_tab, s_slot, t0, head, j); break;
+    case 2: restore_unit<PKV_TAG_K8V8, false, BF16>(a, u, s_tab, s_slot, t0, head, j); break;
+    case 3: restore_unit<PKV_TAG_K8V8, true, BF16>(a, u, s_tab, s_slot, t0, head, j); break;
+    case 4: restore_unit<PKV_TAG_K8V4, false, BF16>(a, u, s_tab, s_slot, t0, head, j); break;
+    case 5: restore_unit<PKV_TAG_K8V4, true, BF16>(a, u, s_tab, s_slot, t0, head, j); break;
+    case 6: restore_unit<PKV_TAG_K4V4, false, BF16>(a, u, s_tab, s_slot, t0, head, j); break;
+    default: restore_unit<PKV_TAG_K4V4, true, BF16>(a, u, s_tab, s_slot, t0, head, j); break;
+  }
+}
+
+bool ranges_overlap(const void* a, uint64_t na, const void* b, uint64_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+}  // namespace
+}  // namespace pkv
+
+struct pkv_plan {
+  pkv::HostPlan host;  // units are dropped after upload; metadata kept
+  void* device_mem = nullptr;
+  pkv::Unit* d_units = nullptr;
+  pkv::ReqDev* d_reqs = nullptr;
+  double* d_tables = nullptr;
+  int32_t* d_page_tables = nullptr;
+  int device = -1;
+};
+
+extern "C" {
+
+pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
+                              pkv_plan_t** out) {
+  if (!out) return PKV_ERR_INVALID_ARGUMENT;
+  *out = nullptr;
+  pkv_plan* plan = new (std::nothrow) pkv_plan();
+  if (!plan) return PKV_ERR_OUT_OF_MEMORY;
+  pkv_status_t st = pkv::build_host_plan(model, requests, num_requests, &plan->host);
+  if (st != PKV_OK) {
+    delete plan;
+    return st;
+  }
+  // Device side: one allocation, 256-byte aligned sections.
+  auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t n_units = plan->host.units.size() * sizeof(pkv::Unit);
+  const size_t n_reqs = plan->host.reqs.size() * sizeof(pkv::ReqDev);
+  const size_t n_tab = plan->host.tables.size() * sizeof(double);
+  const size_t n_pt = plan->host.page_tables.size() * sizeof(int32_t);
+  const size_t total = al(n_units) + al(n_reqs) + al(n_tab) + al(n_pt);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    delete plan;
+    return PKV_ERR_DEVICE;
+  }
+  plan->device = dev;
+  plan->host.info.device = dev;
+  if (total > 0) {
+    hipError_t e = hipMalloc(&plan->device_mem, total);
+    if (e != hipSuccess) {
+      plan->device_mem = nullptr;
+      delete plan;
+      return e == hipErrorOutOfMemory ? PKV_ERR_OUT_OF_MEMORY : PKV_ERR_DEVICE;
+    }
+    char* p = static_cast<char*>(plan->device_mem);
+    plan->d_units = reinterpret_cast<pkv::Unit*>(p);
+    p += al(n_units);
+    plan->d_reqs = reinterpret_cast<pkv::ReqDev*>(p);
+    p += al(n_reqs);
+    plan->d_tables = reinterpret_cast<double*>(p);
+    p += al(n_tab);
+    plan->d_page_tables = reinterpret_cast<int32_t*>(p);
+    bool ok = true;
+    if (n_units) ok = ok && hipMemcpy(plan->d_units, plan->host.units.data(), n_units, hipMemcpyHostToDevice) == hipSuccess;
+    if (n_reqs) ok = ok && hipMemcpy(plan->d_reqs, plan->host.reqs.data(), n_reqs, hipMemcpyHostToDevice) == hipSuccess;
+    if (n_tab) ok = ok && hipMemcpy(plan->d_tables, plan->host.tables.data(), n_tab, hipMemcpyHostToDevice) == hipSuccess;
+    if (n_pt)
+      ok = ok && hipMemcpy(plan->d_page_tables, plan->host.page_tables.data(), n_pt, hipMemcpyHostToDevice) == hipSuccess;
+    if (!ok) {
+      (void)hipFree(plan->device_mem);
+      delete plan;
+      return PKV_ERR_DEVICE;
+    }
+  }
+  // The device copy is authoritative; keep only the metadata on the host.
+  std::vector<pkv::Unit>().swap(plan->host.units);
+  std::vector<double>().swap(plan->host.tables);
+  std::vector<int32_t>().swap(plan->host.page_tables);
+  *out = plan;
+  return PKV_OK;
+}
+
+pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t payload_bytes, const void* scales,
+                         uint64_t scale_bytes, void* k_cache, void* v_cache, uint64_t cache_bytes, void* hip_stream) {
+  if (!plan) return PKV_ERR_INVALID_ARGUMENT;
+  const pkv_plan_info_t& info = plan->host.info;
+  if (info.num_units == 0) return PKV_OK;
+  if (!payload || !scales || !k_cache || !v_cache) return PKV_ERR_INVALID_ARGUMENT;
+  if (reinterpret_cast<uintptr_t>(payload) % 16 || reinterpret_cast<uintptr_t>(scales) % 8 ||
+      reinterpret_cast<uintptr_t>(k_cache) % 16 || reinterpret_cast<uintptr_t>(v_cache) % 16)
+    return PKV_ERR_INVALID_ARGUMENT;
+  if (payload_bytes < info.payload_bytes || scale_bytes < info.scale_bytes || cache_bytes < info.cache_bytes)
+    return PKV_ERR_INVALID_ARGUMENT;
+  const uint64_t cb = info.cache_bytes;
+  if (pkv::ranges_overlap(k_cache, cb, v_cache, cb) || pkv::ranges_overlap(k_cache, cb, payload, info.payload_bytes) ||
+      pkv::ranges_overlap(v_cache, cb, payload, info.payload_bytes) ||
+      pkv::ranges_overlap(k_cache, cb, scales, info.scale_bytes) ||
+      pkv::ranges_overlap(v_cache, cb, scales, info.scale_bytes))
+    return PKV_ERR_INVALID_ARGUMENT;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
+
+  const pkv_model_t& m = plan->host.model;
+  pkv::KernelArgs a;
+  a.units = plan->d_units;
+  a.reqs = plan->d_reqs;
+  a.tables = plan->d_tables;
+  a.page_tables = plan->d_page_tables;
+  a.payload = static_cast<const uint8_t*>(payload);
+  a.scales = static_cast<const uint16_t*>(scales);
+  a.k_cache = static_cast<uint16_t*>(k_cache);
+  a.v_cache = static_cast<uint16_t*>(v_cache);
+  a.layer_elems = m.pool_pages * int64_t(m.page_size) * m.num_kv_heads * m.head_dim;
+  a.H = m.num_kv_heads;
+  a.D = m.head_dim;
+  a.log2P = plan->host.log2_page;
+  a.cols = m.num_kv_heads * m.head_dim / 16;
+  a.tpp = pkv::kWorkgroup / a.cols;
+  const dim3 grid(static_cast<uint32_t>(info.num_units)), block(pkv::kWorkgroup);
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  if (m.out_dtype == PKV_OUT_BF16)
+    hipLaunchKernelGGL(pkv::restore_kernel<true>, grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL(pkv::restore_kernel<false>, grid, block, 0, stream, a);
+  return hipGetLastError() == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
+}
+
+void pkv_free(pkv_plan_t* plan) {
+  if (!plan) return;
+  if (plan->device_mem) {
+    int cur = -1;
+    const bool switched = hipGetDevice(&cur) == hipSuccess && cur != plan->device &&
+                          hipSetDevice(plan->device) == hipSuccess;
+    (void)hipFree(plan->device_mem);
+    if (switched) (void)hipSetDevice(cur);
+  }
+  delete plan;
+}
+
+pkv_status_t pkv_plan_query(const pkv_plan_t* plan, pkv_plan_info_t* info) {
+  if (!plan || !info) return PKV_ERR_INVALID_ARGUMENT;
+  *info = plan->host.info;
+  return PKV_OK;
+}
+
+}  // extern "C"

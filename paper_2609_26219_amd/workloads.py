@@ -156,27 +156,32 @@ def quantize_tiles(x: np.ndarray, n_valid: np.ndarray, bits: int):
     ``x`` is float32 ``[nb, B, H, D]``; rows ``>= n_valid[i]`` of block ``i``
     are padding and excluded from the range.  Zero = min rounded down to fp16,
     scale = (max - zero) / (2^bits - 1) rounded up to fp16, code =
-    rint((x - zero) / scale) clipped to the code range (code 0 when the scale
-    is 0).  The rounding directions keep every element within half a step of
-    its decoded value.  Returns (codes uint8 [nb,B,H,D], scale fp16 [nb,H],
-    zero fp16 [nb,H]).
+    rint((x - zero) / scale) in double precision, clipped to the code range
+    (a zero scale means every valid element equals the zero: code 0).  The
+    rounding directions keep every element within half a step of its decoded
+    value.  Returns (codes uint8 [nb,B,H,D], scale fp16 [nb,H], zero fp16 [nb,H]).
     """
     nb, B, H, D = x.shape
     qmax = (1 << bits) - 1
-    valid = (np.arange(B)[None, :] < n_valid[:, None])  # [nb, B]
-    vmask = valid[:, :, None, None]
-    lo = np.where(vmask, x, np.float32(np.inf)).min(axis=(1, 3)).astype(np.float64)
-    hi = np.where(vmask, x, np.float32(-np.inf)).max(axis=(1, 3)).astype(np.float64)
+    n_valid = np.asarray(n_valid)
+    lo = x.min(axis=(1, 3)).astype(np.float64)
+    hi = x.max(axis=(1, 3)).astype(np.float64)
+    for i in np.nonzero(n_valid < B)[0]:  # partial block: range over valid rows only
+        lo[i] = x[i, :n_valid[i]].min(axis=(0, 2))
+        hi[i] = x[i, :n_valid[i]].max(axis=(0, 2))
     zero = fp16_round_down(lo)
     scale = fp16_round_up((hi - zero.astype(np.float64)) / qmax)
-    s64 = scale.astype(np.float64)[:, None, :, None]
-    z64 = zero.astype(np.float64)[:, None, :, None]
-    safe = np.where(s64 > 0, s64, 1.0)
-    q = np.rint((x.astype(np.float64) - z64) / safe)
-    q = np.where(s64 > 0, q, 0.0)
-    q = np.clip(q, 0, qmax)
-    q = np.where(vmask, q, 0.0)
-    return q.astype(np.uint8), scale, zero
+    s64 = scale.astype(np.float64)
+    s64[s64 == 0] = 1.0
+    q = x.astype(np.float64)
+    q -= zero.astype(np.float64)[:, None, :, None]
+    q /= s64[:, None, :, None]
+    np.rint(q, out=q)
+    np.clip(q, 0, qmax, out=q)
+    codes = q.astype(np.uint8)
+    for i in np.nonzero(n_valid < B)[0]:
+        codes[i, n_valid[i]:] = 0
+    return codes, scale, zero
 
 
 def pack_nibbles(codes: np.ndarray) -> np.ndarray:

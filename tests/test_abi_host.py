@@ -1,0 +1,226 @@
+"""Host-side tests of the C ABI: runs without a GPU.
+
+The library must load and export every function ``include/pkv.h`` declares;
+``pkv_payload_size`` must agree with the oracle's and the generator's own
+layout walks; every argument error of ``pkv_restore_plan`` must be reported
+before any HIP call (so here, on a machine without a GPU)."""
+import copy
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_26219_amd import binding as pb
+from paper_2609_26219_amd import workloads as wl
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "pkv.h")
+
+
+def _gpu_present():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:  # pragma: no cover
+        return False
+
+
+VALID = pb.PKV_OK if _gpu_present() else pb.PKV_ERR_DEVICE
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return pb.load()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pkv_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_what_binding_lists():
+    assert _declared_functions() == sorted(pb.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", pb.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (pkv_\w+)", out))
+    for name in _declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_status_strings(lib):
+    for code in range(-7, 1):
+        assert pb.pkv_status_string(code) != "unknown status"
+    assert pb.pkv_status_string(5) == "unknown status"
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b_1l"])
+def test_payload_size_three_ways(name):
+    case = wl.make_case(name)
+    for tag_map in (None, wl.TAG_K4V4):
+        r = case.requests[0]
+        if tag_map is not None:
+            r = copy.copy(r)
+            r.tags = np.where(r.tags == wl.TAG_K8V4, tag_map, r.tags).astype(np.uint8)
+        lib_bytes, lib_scales = pb.pkv_payload_size(case.shape, r)
+        gen_bytes, gen_scales = wl.encoded_request_nbytes(case.shape, r)
+        assert lib_bytes == gen_bytes == oracle.request_payload_bytes(case.shape, r)
+        assert lib_scales == gen_scales
+
+
+# ---------------------------------------------------------------------------
+# Plan validation
+# ---------------------------------------------------------------------------
+
+def _base():
+    case = wl.make_custom(3, L=2, H=2, D=64, B=16, P=16, n_tokens=(100, 40), deltas=(5, -3), rho0s=(20, 7),
+                          repair_frac=0.0)
+    return case.shape, [copy.copy(r) for r in case.requests]
+
+
+def _status(shape, reqs):
+    return pb.pkv_restore_plan_status(shape, reqs)
+
+
+def test_valid_plan_passes_validation():
+    shape, reqs = _base()
+    assert _status(shape, reqs) == VALID
+    assert _status(shape, []) == VALID
+
+
+@pytest.mark.parametrize("field,value", [
+    ("head_dim", 72), ("head_dim", 8), ("head_dim", 1024), ("num_kv_heads", 0), ("num_layers", 0),
+    ("page_size", 12), ("page_size", 0), ("pool_pages", 0), ("rope_theta", 0.0), ("rope_theta", float("nan")),
+    ("out_dtype", 2), ("block_tokens", 0), ("block_tokens", 2048), ("num_kv_heads", 65),
+])
+def test_bad_model(field, value):
+    shape, reqs = _base()
+    import dataclasses
+    shape = dataclasses.replace(shape, **{field: value})
+    assert _status(shape, reqs) == pb.PKV_ERR_INVALID_ARGUMENT
+
+
+def test_tile_alignment_rule():
+    import dataclasses
+    shape, reqs = _base()
+    # B*H*D % 32 != 0 -> rejected (B=1, H=1, D=16)
+    shape = dataclasses.replace(shape, block_tokens=1, num_kv_heads=1, head_dim=16)
+    for r in reqs:
+        nb = wl.num_blocks(r.suffix_tokens, 1)
+        r.tags = np.zeros(nb, np.uint8)
+        r.repair = np.zeros(nb, np.uint8)
+    assert _status(shape, reqs) == pb.PKV_ERR_INVALID_ARGUMENT
+
+
+def test_bad_tag():
+    shape, reqs = _base()
+    reqs[1].tags = reqs[1].tags.copy()
+    reqs[1].tags[1] = 4
+    assert _status(shape, reqs) == pb.PKV_ERR_BAD_TAG
+
+
+def test_bad_tag_in_repair_block_still_rejected():
+    shape, reqs = _base()
+    reqs[0].tags = reqs[0].tags.copy()
+    reqs[0].repair = reqs[0].repair.copy()
+    reqs[0].tags[2] = 9
+    reqs[0].repair[2] = 1
+    assert _status(shape, reqs) == pb.PKV_ERR_BAD_TAG
+
+
+@pytest.mark.parametrize("field,value", [
+    ("reserved", 1), ("payload_offset", 8), ("scale_offset", 2), ("suffix_tokens", -1), ("dst_row0", -5),
+])
+def test_bad_request_fields(field, value):
+    shape, reqs = _base()
+    setattr(reqs[0], field, value)
+    assert _status(shape, reqs) == pb.PKV_ERR_INVALID_ARGUMENT
+
+
+def _first_f_page(shape, req):
+    b = int(np.nonzero(req.repair == 0)[0][0])
+    return (req.dst_row0 + b * shape.block_tokens) // shape.page_size
+
+
+def test_page_out_of_range():
+    shape, reqs = _base()
+    reqs[0].page_table = reqs[0].page_table.copy()
+    reqs[0].page_table[_first_f_page(shape, reqs[0])] = shape.pool_pages
+    assert _status(shape, reqs) == pb.PKV_ERR_PAGE_OUT_OF_RANGE
+    reqs[0].page_table[_first_f_page(shape, reqs[0])] = -2
+    assert _status(shape, reqs) == pb.PKV_ERR_PAGE_OUT_OF_RANGE
+
+
+def test_rows_past_page_table():
+    shape, reqs = _base()
+    reqs[1].page_table = reqs[1].page_table[:1].copy()
+    assert _status(shape, reqs) == pb.PKV_ERR_PAGE_OUT_OF_RANGE
+
+
+def test_page_unmapped():
+    shape, reqs = _base()
+    reqs[0].page_table = reqs[0].page_table.copy()
+    last_row = reqs[0].dst_row0 + reqs[0].suffix_tokens - 1
+    reqs[0].page_table[last_row // shape.page_size] = -1
+    assert _status(shape, reqs) == pb.PKV_ERR_PAGE_UNMAPPED
+
+
+def test_unmapped_pages_of_repair_blocks_and_prefix_are_fine():
+    shape, reqs = _base()
+    r = reqs[0]
+    r.repair = np.zeros_like(r.repair)
+    r.repair[0] = 1
+    r.page_table = r.page_table.copy()
+    # Pages holding only prefix rows or rows of repair block 0: unmap them.
+    first_f_row = r.dst_row0 + shape.block_tokens
+    for lp in range(first_f_row // shape.page_size):
+        r.page_table[lp] = -1
+    assert _status(shape, reqs) == VALID
+
+
+def test_page_alias_within_request():
+    shape, reqs = _base()
+    r = reqs[0]
+    r.page_table = r.page_table.copy()
+    lp = _first_f_page(shape, r)
+    r.page_table[lp + 1] = r.page_table[lp]
+    assert _status(shape, reqs) == pb.PKV_ERR_PAGE_ALIAS
+
+
+def test_page_alias_across_requests():
+    shape, reqs = _base()
+    reqs[1].page_table = reqs[1].page_table.copy()
+    reqs[1].page_table[_first_f_page(shape, reqs[1])] = reqs[0].page_table[_first_f_page(shape, reqs[0])]
+    assert _status(shape, reqs) == pb.PKV_ERR_PAGE_ALIAS
+
+
+def test_null_pointers(lib):
+    import ctypes
+    shape, reqs = _base()
+    m = pb.make_model(shape)
+    arr = pb._Requests(reqs)
+    out = ctypes.c_void_p()
+    assert lib.pkv_restore_plan(None, arr.array, arr.count, ctypes.byref(out)) == pb.PKV_ERR_INVALID_ARGUMENT
+    assert lib.pkv_restore_plan(ctypes.byref(m), None, 1, ctypes.byref(out)) == pb.PKV_ERR_INVALID_ARGUMENT
+    assert lib.pkv_restore_plan(ctypes.byref(m), arr.array, arr.count, None) == pb.PKV_ERR_INVALID_ARGUMENT
+    assert lib.pkv_restore_plan(ctypes.byref(m), arr.array, -1, ctypes.byref(out)) == pb.PKV_ERR_INVALID_ARGUMENT
+    arr.array[0].tags = None
+    assert lib.pkv_restore_plan(ctypes.byref(m), arr.array, arr.count, ctypes.byref(out)) == pb.PKV_ERR_INVALID_ARGUMENT
+    assert out.value is None
+    lib.pkv_free(None)  # no-op
+    assert lib.pkv_restore(None, None, 0, None, 0, None, None, 0, None) == pb.PKV_ERR_INVALID_ARGUMENT
+
+
+def test_empty_suffix_and_all_repair_are_valid():
+    shape, reqs = _base()
+    reqs[0].suffix_tokens = 0
+    reqs[0].tags = np.zeros(0, np.uint8)
+    reqs[0].repair = np.zeros(0, np.uint8)
+    reqs[1].repair = np.ones_like(reqs[1].repair)
+    reqs[1].page_table = np.full_like(reqs[1].page_table, -1)
+    assert _status(shape, reqs) == VALID

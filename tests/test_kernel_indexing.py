@@ -1,0 +1,127 @@
+"""CPU emulation of the kernel's address arithmetic (no GPU).
+
+Takes the work list the host plan builds (through an internal test hook of
+libpkv), replays the thread -> (token, head, piece) mapping and the address
+formulas of ``restore.hip`` for every thread of every workgroup, and checks:
+every read stays inside the payload/scales and inside the valid rows of a
+reused block's tiles; every write stays inside the caches; every element of
+every restored row is written exactly once and nothing else is written.
+Keep the constants below in step with the kernel's launch code.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_26219_amd import binding as pb
+from paper_2609_26219_amd import workloads as wl
+
+WG = 256  # threads per workgroup
+KBITS = (16, 8, 8, 4)
+VBITS = (16, 8, 4, 4)
+UNIT_DTYPE = np.dtype([("k_off", "<u8"), ("v_off", "<u8"), ("scale_off", "<u8"), ("row0", "<i8"),
+                       ("layer", "<i4"), ("req", "<i4"), ("tag", "<i4"), ("n_valid", "<i4")])
+
+
+def host_units(shape, requests):
+    lib = pb.load()
+    fn = lib.pkv_internal_host_units
+    fn.argtypes = [ctypes.POINTER(pb.PkvModel), ctypes.POINTER(pb.PkvRequest), ctypes.c_int32, ctypes.c_void_p,
+                   ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
+    fn.restype = ctypes.c_int32
+    m = pb.make_model(shape)
+    reqs = pb._Requests(requests)
+    count = ctypes.c_int64()
+    assert fn(ctypes.byref(m), reqs.array, reqs.count, None, 0, ctypes.byref(count)) == 0
+    units = np.zeros(count.value, dtype=UNIT_DTYPE)
+    assert fn(ctypes.byref(m), reqs.array, reqs.count, units.ctypes.data, count.value, ctypes.byref(count)) == 0
+    return units
+
+
+def emulate(case):
+    s = case.shape
+    H, D, B, P = s.num_kv_heads, s.head_dim, s.block_tokens, s.page_size
+    cols = H * D // 16
+    tpp = WG // cols
+    dq = D // 16
+    layer_elems = s.pool_pages * P * H * D
+    cache_elems = s.num_layers * layer_elems
+    units = host_units(s, case.requests)
+    tid = np.arange(WG)
+    t0 = tid // cols
+    active = t0 < tpp
+    c = tid % cols
+    head = c // dq
+    j = c % dq
+    writes_k = np.zeros(cache_elems, dtype=np.int32)
+    writes_v = np.zeros(cache_elems, dtype=np.int32)
+    payload_read = np.zeros(case.payload_nbytes, dtype=bool)
+    # allowed payload bytes: valid rows of reused blocks' tiles
+    allowed = np.zeros(case.payload_nbytes, dtype=bool)
+    for ri, r in enumerate(case.requests):
+        offsets, layer_bytes = oracle.block_layout(r.tags, B, H, D)
+        for layer in range(s.num_layers):
+            for b in oracle.reused_blocks(r):
+                n = oracle.valid_tokens(r, B, b)
+                ko, vo = offsets[b]
+                base = r.payload_offset + layer * layer_bytes
+                t = int(r.tags[b])
+                allowed[base + ko: base + ko + n * H * D * KBITS[t] // 8] = True
+                allowed[base + vo: base + vo + n * H * D * VBITS[t] // 8] = True
+    assert len(units) == sum(len(oracle.reused_blocks(r)) for r in case.requests) * s.num_layers
+    for u in units:
+        r = case.requests[u["req"]]
+        n_valid = int(u["n_valid"])
+        assert 1 <= n_valid <= B <= 1024 and D <= 512
+        rows = u["row0"] + np.arange(n_valid)
+        lp = rows >> int(np.log2(P))
+        assert (lp < len(r.page_table)).all()
+        page = r.page_table[lp].astype(np.int64)
+        assert ((page >= 0) & (page < s.pool_pages)).all()
+        s_slot = int(u["layer"]) * layer_elems + (page * P + (rows & (P - 1))) * H * D
+        tag = int(u["tag"])
+        kb, vb = KBITS[tag], VBITS[tag]
+        if tag != 0:
+            sc = int(u["scale_off"]) + 4 * head[active]
+            assert (sc >= 0).all() and (sc + 4 <= case.scale_elems).all()
+        for tt in range(tpp):
+            sel = active & (t0 == tt)
+            for t in range(tt, n_valid, tpp):
+                rr = t * H + head[sel]
+                krow = int(u["k_off"]) + rr * (D * kb // 8)
+                vrow = int(u["v_off"]) + rr * (D * vb // 8)
+                for start, length in ((krow + 8 * j[sel] * kb // 8, kb), (krow + (D // 2 + 8 * j[sel]) * kb // 8, kb),
+                                      (vrow + 16 * j[sel] * vb // 8, 2 * vb)):
+                    for st in start:
+                        assert 0 <= st and st + length <= case.payload_nbytes
+                        payload_read[st: st + length] = True
+                dst = s_slot[t] + head[sel] * D
+                for off in (8 * j[sel], D // 2 + 8 * j[sel]):
+                    for d0 in dst + off:
+                        assert 0 <= d0 and d0 + 8 <= cache_elems
+                        writes_k[d0: d0 + 8] += 1
+                for d0 in dst + 16 * j[sel]:
+                    writes_v[d0: d0 + 16] += 1
+    assert not (payload_read & ~allowed).any(), "read outside the valid rows of reused blocks"
+    assert (payload_read == allowed).all(), "some restored payload byte is never read"
+    written = oracle.written_slots(s, case.requests)
+    want = np.repeat(np.tile(written, s.num_layers), H * D).astype(np.int32)
+    assert np.array_equal(writes_k, want), "K writes differ from the restored rows"
+    assert np.array_equal(writes_v, want), "V writes differ from the restored rows"
+
+
+@pytest.mark.parametrize("maker", [
+    lambda: wl.make_case("tiny"),
+    lambda: wl.make_case("tiny", int4_tag=wl.TAG_K4V4),
+    lambda: wl.make_custom(1, L=2, H=3, D=128, B=32, P=16, n_tokens=(70,), deltas=(12,), rho0s=(9,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2),
+    lambda: wl.make_custom(2, L=1, H=8, D=64, B=4, P=16, n_tokens=(23, 9), deltas=(5, 0), rho0s=(2, 40),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2),
+    lambda: wl.make_custom(3, L=2, H=2, D=256, B=64, P=32, n_tokens=(130,), deltas=(-9,), rho0s=(31,),
+                           tag_set=(0, 2), mix=(1, 1), repair_frac=0.1),
+    lambda: wl.make_custom(4, L=1, H=32, D=128, B=8, P=8, n_tokens=(41,), deltas=(3,), rho0s=(5,),
+                           tag_set=(1, 2), mix=(1, 1), repair_frac=0.0),
+], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "d256_b64", "h32_b8"])
+def test_kernel_addresses(maker):
+    emulate(maker())

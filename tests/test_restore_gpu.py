@@ -1,0 +1,163 @@
+"""GPU parity of the HIP restore against the CPU oracle, through the C ABI."""
+import copy
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_26219_amd import binding as pb
+from paper_2609_26219_amd import workloads as wl
+
+from parity import check_full, check_sampled, log
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _t
+    if not _t.cuda.is_available():
+        pytest.skip("no GPU")
+    pb.load()
+    return _t
+
+
+def _run(case, torch):
+    from paper_2609_26219_amd.device import DeviceRestore
+    dr = DeviceRestore(case)
+    dr.run()
+    torch.cuda.synchronize()
+    return dr
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b_1l"])
+def test_named_small_full(name, torch):
+    log(f"[gpu] {name}: full-cache parity")
+    dr = _run(wl.make_case(name), torch)
+    st = check_full(dr)
+    log(f"  {st}")
+    assert st.bit_exact_fraction > 0.9999
+
+
+def test_tiny_k4v4_reading(torch):
+    dr = _run(wl.make_case("tiny", int4_tag=wl.TAG_K4V4), torch)
+    check_full(dr)
+
+
+PROPERTY_CASES = [
+    # (B, P, D, H, n_tokens, deltas, rho0s, tag_set, repair_frac, out)
+    (8, 8, 64, 2, (61,), (3,), (0,), (0, 1, 2, 3), 0.2, wl.OUT_FP16),
+    (16, 16, 128, 1, (200,), (-77,), (16,), (2,), 0.0, wl.OUT_BF16),
+    (32, 16, 128, 4, (150,), (0,), (5,), (0, 1, 2), 0.3, wl.OUT_BF16),
+    (64, 32, 64, 2, (130,), (9999,), (31,), (1, 3), 0.1, wl.OUT_FP16),
+    (32, 8, 64, 8, (97, 33, 256), (1, -1, 8192), (3, 64, 1000), (0, 1, 2, 3), 0.25, wl.OUT_BF16),
+    (16, 32, 256, 2, (45,), (-8192,), (17,), (0, 2), 0.0, wl.OUT_FP16),
+    (32, 16, 128, 3, (70,), (12,), (9,), (0, 1, 2, 3), 0.0, wl.OUT_BF16),  # H*D/16 = 24 (idle lanes)
+    (4, 16, 128, 8, (23,), (5,), (2,), (0, 1, 2, 3), 0.2, wl.OUT_FP16),
+]
+
+
+@pytest.mark.parametrize("params", PROPERTY_CASES, ids=[f"case{i}" for i in range(len(PROPERTY_CASES))])
+def test_property_cases(params, torch):
+    B, P, D, H, n, deltas, rho0s, tags, rep, out = params
+    case = wl.make_custom(hash(params) & 0xFFFF, L=2, H=H, D=D, B=B, P=P, n_tokens=n, deltas=deltas, rho0s=rho0s,
+                          tag_set=tags, mix=[1.0] * len(tags), repair_frac=rep, out_dtype=out, outlier_pairs=1)
+    log(f"[gpu] property case {params}")
+    check_full(_run(case, torch))
+
+
+def test_all_repair_writes_nothing(torch):
+    case = wl.make_custom(21, L=2, n_tokens=(64, 20), deltas=(4, 2), repair_all=True)
+    dr = _run(case, torch)
+    assert dr.info["num_units"] == 0
+    k, v = dr.host_caches()
+    assert np.array_equal(k, case.host_prefill(0)) and np.array_equal(v, case.host_prefill(1))
+
+
+def test_fp16_tag_zero_shift_is_bit_copy(torch):
+    case = wl.make_custom(22, H=8, D=128, B=32, P=16, n_tokens=(300,), deltas=(0,), rho0s=(13,),
+                          tag_set=(wl.TAG_FP16,), mix=(1.0,), repair_frac=0.1, out_dtype=wl.OUT_FP16)
+    st = check_full(_run(case, torch))
+    assert st.n_bit_exact == st.n
+
+
+def test_restore_is_repeatable_and_plan_reusable(torch):
+    from paper_2609_26219_amd.device import DeviceRestore
+    case = wl.make_case("tiny")
+    dr = DeviceRestore(case)
+    dr.run()
+    dr.run()
+    torch.cuda.synchronize()
+    k1, v1 = dr.host_caches()
+    # same plan, a second pair of caches
+    k2 = torch.zeros_like(dr.k_cache)
+    v2 = torch.zeros_like(dr.v_cache)
+    pb.restore_tensors(dr.plan, dr.payload, dr.scales, k2, v2)
+    torch.cuda.synchronize()
+    written = oracle.written_slots(case.shape, case.requests)
+    s = case.shape
+    a = k2.cpu().numpy().view(np.uint16).reshape(s.num_layers, s.pool_slots, -1)
+    b = k1.reshape(a.shape)
+    assert np.array_equal(a[:, written], b[:, written])
+    assert (a[:, ~written] == 0).all()
+    check_full(dr)
+
+
+def test_restore_argument_errors(torch):
+    from paper_2609_26219_amd.device import DeviceRestore
+    dr = DeviceRestore(wl.make_case("tiny"))
+    nb = lambda t: t.numel() * t.element_size()
+    p, s, k, v = dr.payload, dr.scales, dr.k_cache, dr.v_cache
+    good = (p.data_ptr(), nb(p), s.data_ptr(), nb(s), k.data_ptr(), v.data_ptr(), nb(k), 0)
+    assert pb.pkv_restore_status(dr.plan, *good) == pb.PKV_OK
+    torch.cuda.synchronize()
+    bad = [
+        (p.data_ptr(), nb(p) - 16) + good[2:],                     # payload too small
+        good[:3] + (nb(s) - 2,) + good[4:],                        # scales too small
+        good[:6] + (nb(k) - 2, 0),                                 # cache too small
+        good[:4] + (k.data_ptr(), k.data_ptr()) + good[6:],        # K and V alias
+        (p.data_ptr() + 1,) + good[1:],                            # misaligned payload
+        good[:4] + (k.data_ptr() + 2,) + good[5:],                 # misaligned cache
+        good[:4] + (p.data_ptr(),) + good[5:],                     # cache overlaps payload
+        (0,) + good[1:],                                           # null payload
+    ]
+    for args in bad:
+        assert pb.pkv_restore_status(dr.plan, *args) == pb.PKV_ERR_INVALID_ARGUMENT, args
+    check_full(dr)  # nothing above wrote anything
+
+
+def test_streams(torch):
+    from paper_2609_26219_amd.device import DeviceRestore
+    dr = DeviceRestore(wl.make_case("llama8b_1l"))
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        dr.run()
+    s.synchronize()
+    check_full(dr)
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, sampled outputs
+# ---------------------------------------------------------------------------
+
+def test_llama8b_32l_full_size(torch):
+    log("[gpu] llama8b_32l: full-size restore, 3 sampled layers + untouched check")
+    case = wl.make_case("llama8b_32l")
+    dr = _run(case, torch)
+    st = check_sampled(dr, [(0, 0), (0, 17), (0, 31)])
+    log(f"  {st}")
+
+
+def test_llama70b_full_size(torch):
+    log("[gpu] llama70b: full-size restore, 2 sampled layers + untouched check")
+    case = wl.make_case("llama70b", distinct_layers=2)
+    dr = _run(case, torch)
+    check_sampled(dr, [(0, 1), (0, 78)])
+
+
+def test_batched16_full_size(torch):
+    log("[gpu] batched16: 16 requests on a 2^20-slot pool, 4 sampled (request, layer) + untouched check")
+    case = wl.make_case("batched16", distinct_layers=1)
+    dr = _run(case, torch)
+    check_sampled(dr, [(0, 0), (5, 13), (11, 31), (15, 7)])

@@ -92,7 +92,7 @@ def _oracle_layer(args):
     return time.perf_counter() - t
 
 
-def cpu_baseline(case, max_workers: int = 16, target_layers: int = 16):
+def cpu_baseline(case, max_workers: int = 16, target_layers: int = 32):
     """Oracle throughput on the host cores over a bounded sample of layers."""
     global _CPU_CASE
     _CPU_CASE = case

@@ -14,40 +14,42 @@ constexpr int kMaxHeadDim = 512;
 constexpr int kMaxRowElems = 4096;   // num_kv_heads * head_dim
 constexpr int kMaxBlockTokens = 1024;
 constexpr int kWorkgroup = 256;       // threads per workgroup
+// Target output per unit: units of about 16K elements per cache (32 KiB of
+// binary16/bfloat16) keep workgroups short, so the launch drains evenly.
+constexpr int kUnitElems = 16384;
 
 // Key / value bits per channel of each tag (Eq. 14 tiers plus uniform 4-bit).
 constexpr int kKeyBits[4] = {16, 8, 8, 4};
 constexpr int kValueBits[4] = {16, 8, 4, 4};
 
-// One workgroup's work: every head of one reused block of one layer of one
-// request.  48 bytes.
+// One workgroup's work: every head of up to `n_valid` consecutive tokens of
+// one reused block of one layer of one request.  64 bytes.
 struct Unit {
-  uint64_t k_off;      // byte offset of the block's K tile in the payload
-  uint64_t v_off;      // byte offset of its V tile
-  uint64_t scale_off;  // binary16-element offset of its (head 0, K, scale) entry
-  int64_t row0;        // logical destination row of the block's first token
+  uint64_t k_off;      // byte offset of the unit's first K row in the payload
+  uint64_t v_off;      // byte offset of its first V row
+  uint64_t scale_off;  // binary16-element offset of the block's (head 0, K, scale) entry
+  int64_t row0;        // logical destination row of the unit's first token
+  int64_t pt_off;      // offset, in int32, of the request's page table
+  int32_t table_off;   // offset, in doubles, of the request's [D/2][2] (cos, sin) table
   int32_t layer;
-  int32_t req;
-  int32_t tag;
-  int32_t n_valid;     // valid tokens in the block (< B only for the last block)
-};
-static_assert(sizeof(Unit) == 48, "Unit layout");
-
-// Per-request device metadata.  32 bytes.
-struct ReqDev {
-  int64_t table_off;  // offset, in doubles, of the request's [D/2][2] (cos, sin) table
-  int64_t pt_off;     // offset, in int32, of the request's page table
-  int32_t rotate;     // Delta != 0
-  int32_t num_logical_pages;
+  int32_t tag;         // bits 0-7: pkv_tag_t; bit 8: rotate keys (Delta != 0)
+  int32_t n_valid;     // tokens in the unit
   int64_t reserved;
 };
-static_assert(sizeof(ReqDev) == 32, "ReqDev layout");
+static_assert(sizeof(Unit) == 64, "Unit layout");
+constexpr int32_t kUnitRotate = 1 << 8;
+
+// Per-request metadata kept on the host.
+struct ReqInfo {
+  int64_t table_off;  // offset, in doubles, of the request's table
+  int64_t pt_off;     // offset, in int32, of the request's page table
+};
 
 // Everything the plan needs on the device, built on the host.
 struct HostPlan {
   pkv_model_t model;
   std::vector<Unit> units;
-  std::vector<ReqDev> reqs;
+  std::vector<ReqInfo> reqs;
   std::vector<double> tables;      // per request [D/2][2]
   std::vector<int32_t> page_tables;
   pkv_plan_info_t info;
@@ -60,6 +62,9 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
 
 // Bytes of one layer of a request's checkpoint (tags already validated).
 uint64_t layer_payload_bytes(const pkv_model_t& m, const uint8_t* tags, int64_t nb);
+
+// Tokens per unit for a model: about kUnitElems output elements, at most one block.
+int32_t unit_tokens(const pkv_model_t& m);
 
 }  // namespace pkv
 

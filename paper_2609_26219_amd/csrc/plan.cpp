@@ -67,6 +67,11 @@ uint64_t tile_bytes(const pkv_model_t& m, int bits) {
 
 }  // namespace
 
+int32_t unit_tokens(const pkv_model_t& m) {
+  const int64_t per = kUnitElems / (int64_t(m.num_kv_heads) * m.head_dim);
+  return int32_t(std::max<int64_t>(1, std::min<int64_t>(per, m.block_tokens)));
+}
+
 uint64_t layer_payload_bytes(const pkv_model_t& m, const uint8_t* tags, int64_t nb) {
   uint64_t total = 0;
   for (int64_t b = 0; b < nb; ++b) total += tile_bytes(m, kKeyBits[tags[b]]) + tile_bytes(m, kValueBits[tags[b]]);
@@ -131,18 +136,16 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
   hp.info.num_requests = num_requests;
   hp.info.cache_bytes = uint64_t(L) * uint64_t(m.pool_pages) * uint64_t(P) * uint64_t(H) * uint64_t(D) * 2;
 
+  if (int64_t(num_requests) * D > std::numeric_limits<int32_t>::max()) return PKV_ERR_INVALID_ARGUMENT;
   try {
     hp.reqs.resize(num_requests);
     hp.tables.resize(size_t(num_requests) * size_t(D));
     for (int32_t r = 0; r < num_requests; ++r) {
       const pkv_request_t& q = requests[r];
       const int64_t nb = ceil_div(q.suffix_tokens, B);
-      ReqDev& rd = hp.reqs[r];
+      ReqInfo& rd = hp.reqs[r];
       rd.table_off = int64_t(r) * D;
       rd.pt_off = int64_t(hp.page_tables.size());
-      rd.rotate = q.delta != 0;
-      rd.num_logical_pages = q.num_logical_pages;
-      rd.reserved = 0;
       hp.page_tables.insert(hp.page_tables.end(), q.page_table, q.page_table + q.num_logical_pages);
       // cos / sin of Delta * theta^(-2i/D), in double precision.
       for (int64_t i = 0; i < D / 2; ++i) {
@@ -161,6 +164,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
             pos += tile_bytes(m, kKeyBits[tag]) + tile_bytes(m, kValueBits[tag]);
           }
       const uint64_t layer_bytes = pos;
+      const int64_t per_unit = unit_tokens(m);
       hp.info.payload_bytes = std::max<uint64_t>(hp.info.payload_bytes, q.payload_offset + uint64_t(L) * layer_bytes);
       hp.info.scale_bytes =
           std::max<uint64_t>(hp.info.scale_bytes, (q.scale_offset + uint64_t(L) * nb * H * 4) * 2);
@@ -169,16 +173,22 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
           if (q.repair_mask[b]) continue;
           const int tag = q.tags[b];
           const int64_t n_valid = std::min<int64_t>(B, q.suffix_tokens - b * B);
-          Unit u;
-          u.k_off = q.payload_offset + uint64_t(l) * layer_bytes + block_off[b];
-          u.v_off = u.k_off + tile_bytes(m, kKeyBits[tag]);
-          u.scale_off = q.scale_offset + (uint64_t(l) * nb + b) * H * 4;
-          u.row0 = q.dst_row0 + b * B;
-          u.layer = int32_t(l);
-          u.req = r;
-          u.tag = tag;
-          u.n_valid = int32_t(n_valid);
-          hp.units.push_back(u);
+          // Split the block into units of at most `per_unit` tokens.
+          for (int64_t t0 = 0; t0 < n_valid; t0 += per_unit) {
+            Unit u;
+            const uint64_t block_base = q.payload_offset + uint64_t(l) * layer_bytes + block_off[b];
+            u.k_off = block_base + uint64_t(t0) * H * D * kKeyBits[tag] / 8;
+            u.v_off = block_base + tile_bytes(m, kKeyBits[tag]) + uint64_t(t0) * H * D * kValueBits[tag] / 8;
+            u.scale_off = q.scale_offset + (uint64_t(l) * nb + b) * H * 4;
+            u.row0 = q.dst_row0 + b * B + t0;
+            u.pt_off = rd.pt_off;
+            u.table_off = int32_t(rd.table_off);
+            u.layer = int32_t(l);
+            u.tag = tag | (q.delta != 0 ? kUnitRotate : 0);
+            u.n_valid = int32_t(std::min<int64_t>(per_unit, n_valid - t0));
+            u.reserved = 0;
+            hp.units.push_back(u);
+          }
           hp.info.restored_rows += n_valid;
           hp.info.bytes_read += uint64_t(n_valid) * H * D * (kKeyBits[tag] + kValueBits[tag]) / 8;
           if (tag != PKV_TAG_FP16) hp.info.bytes_read += uint64_t(H) * 4 * 2;

@@ -20,8 +20,10 @@ from paper_2609_26219_amd import workloads as wl
 WG = 256  # threads per workgroup
 KBITS = (16, 8, 8, 4)
 VBITS = (16, 8, 4, 4)
-UNIT_DTYPE = np.dtype([("k_off", "<u8"), ("v_off", "<u8"), ("scale_off", "<u8"), ("row0", "<i8"),
-                       ("layer", "<i4"), ("req", "<i4"), ("tag", "<i4"), ("n_valid", "<i4")])
+UNIT_ELEMS = 16384  # target output elements per unit
+UNIT_DTYPE = np.dtype([("k_off", "<u8"), ("v_off", "<u8"), ("scale_off", "<u8"), ("row0", "<i8"), ("pt_off", "<i8"),
+                       ("table_off", "<i4"), ("layer", "<i4"), ("tag", "<i4"), ("n_valid", "<i4"),
+                       ("reserved", "<i8")])
 
 
 def host_units(shape, requests):
@@ -69,18 +71,27 @@ def emulate(case):
                 t = int(r.tags[b])
                 allowed[base + ko: base + ko + n * H * D * KBITS[t] // 8] = True
                 allowed[base + vo: base + vo + n * H * D * VBITS[t] // 8] = True
-    assert len(units) == sum(len(oracle.reused_blocks(r)) for r in case.requests) * s.num_layers
+    per_unit = max(1, min(B, UNIT_ELEMS // (H * D)))
+    n_units = sum(-(-oracle.valid_tokens(r, B, b) // per_unit) for r in case.requests for b in oracle.reused_blocks(r))
+    assert len(units) == n_units * s.num_layers
+    pt_all = np.concatenate([r.page_table for r in case.requests]).astype(np.int64)
+    pt_start = np.cumsum([0] + [len(r.page_table) for r in case.requests])
     for u in units:
-        r = case.requests[u["req"]]
         n_valid = int(u["n_valid"])
-        assert 1 <= n_valid <= B <= 1024 and D <= 512
+        assert 1 <= n_valid <= per_unit
+        ri = int(np.searchsorted(pt_start, int(u["pt_off"]), side="right") - 1)
+        assert pt_start[ri] == u["pt_off"]
+        r = case.requests[ri]
+        tag = int(u["tag"]) & 0xFF
+        rot = (int(u["tag"]) >> 8) & 1
+        assert rot == int(r.delta != 0)
+        assert u["table_off"] == ri * D  # (cos, sin) table of this request, D doubles
         rows = u["row0"] + np.arange(n_valid)
         lp = rows >> int(np.log2(P))
         assert (lp < len(r.page_table)).all()
-        page = r.page_table[lp].astype(np.int64)
+        page = pt_all[u["pt_off"] + lp]
         assert ((page >= 0) & (page < s.pool_pages)).all()
-        s_slot = int(u["layer"]) * layer_elems + (page * P + (rows & (P - 1))) * H * D
-        tag = int(u["tag"])
+        dst_row = int(u["layer"]) * layer_elems + ((page << int(np.log2(P))) | (rows & (P - 1))) * H * D
         kb, vb = KBITS[tag], VBITS[tag]
         if tag != 0:
             sc = int(u["scale_off"]) + 4 * head[active]
@@ -91,18 +102,17 @@ def emulate(case):
                 rr = t * H + head[sel]
                 krow = int(u["k_off"]) + rr * (D * kb // 8)
                 vrow = int(u["v_off"]) + rr * (D * vb // 8)
-                for start, length in ((krow + 8 * j[sel] * kb // 8, kb), (krow + (D // 2 + 8 * j[sel]) * kb // 8, kb),
-                                      (vrow + 16 * j[sel] * vb // 8, 2 * vb)):
-                    for st in start:
-                        assert 0 <= st and st + length <= case.payload_nbytes
-                        payload_read[st: st + length] = True
-                dst = s_slot[t] + head[sel] * D
+                for base, bits in ((krow, kb), (vrow, vb)):
+                    for start in (base + 8 * j[sel] * bits // 8, base + (D // 2 + 8 * j[sel]) * bits // 8):
+                        for st in start:
+                            assert 0 <= st and st + bits <= case.payload_nbytes
+                            payload_read[st: st + bits] = True
+                dst = dst_row[t] + head[sel] * D
                 for off in (8 * j[sel], D // 2 + 8 * j[sel]):
                     for d0 in dst + off:
                         assert 0 <= d0 and d0 + 8 <= cache_elems
                         writes_k[d0: d0 + 8] += 1
-                for d0 in dst + 16 * j[sel]:
-                    writes_v[d0: d0 + 16] += 1
+                        writes_v[d0: d0 + 8] += 1
     assert not (payload_read & ~allowed).any(), "read outside the valid rows of reused blocks"
     assert (payload_read == allowed).all(), "some restored payload byte is never read"
     written = oracle.written_slots(s, case.requests)
@@ -122,6 +132,8 @@ def emulate(case):
                            tag_set=(0, 2), mix=(1, 1), repair_frac=0.1),
     lambda: wl.make_custom(4, L=1, H=32, D=128, B=8, P=8, n_tokens=(41,), deltas=(3,), rho0s=(5,),
                            tag_set=(1, 2), mix=(1, 1), repair_frac=0.0),
-], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "d256_b64", "h32_b8"])
+    lambda: wl.make_custom(5, L=2, H=8, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2),
+], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "d256_b64", "h32_b8", "h8_d128_split_units"])
 def test_kernel_addresses(maker):
     emulate(maker())

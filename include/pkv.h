@@ -157,8 +157,61 @@ pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t p
  * make sure no enqueued restore still uses it. */
 void pkv_free(pkv_plan_t* plan);
 
+/* ----------------------------------------------------------------------------
+ * Checkpoint write (the offload side, Section IV-D): quantize-and-gather.
+ *
+ * Reads every block of each request's suffix from the OLD context's paged
+ * caches (k_cache / v_cache, [L][pool_pages][P][H][D] of model->out_dtype)
+ * and writes the checkpoint in the format above, which pkv_restore reads:
+ *   FP16 tag: the binary16 value nearest (round to nearest even) to each
+ *     cache value; 8/4-bit tags, per (layer, block, head, K|V) over the valid
+ *     rows: zero = the largest binary16 <= min, scale = the smallest binary16
+ *     >= (max - zero)/(2^bits - 1), code = round-half-even((x - zero)/scale)
+ *     clipped to [0, 2^bits - 1] (code 0 when the scale is 0), so every value
+ *     decodes within scale/2.  Padding rows of a partial last block are
+ *     written as code 0 / +0.  Scale entries of FP16 blocks are written 0.
+ *   Values must be finite, and within the binary16 range (|x| <= 65504) for
+ *     quantized tags, so that zero and scale are binary16 numbers.
+ * The repair set is not known when a checkpoint is written, so every block
+ * is encoded.
+ * ---------------------------------------------------------------------------- */
+typedef struct {
+  int32_t suffix_tokens;      /* N >= 0 */
+  int32_t reserved;           /* must be 0 */
+  int64_t src_row0;           /* omega_0 >= 0: old logical row of suffix token 0 */
+  const uint8_t* tags;        /* host [NB] pkv_tag_t (frozen per-block precision tags) */
+  const int32_t* page_table;  /* host [num_logical_pages] of the old context, -1 = unmapped */
+  int32_t num_logical_pages;  /* >= 0 */
+  int32_t reserved2;          /* must be 0 */
+  uint64_t payload_offset;    /* bytes, % 16 == 0; request payload ranges must not overlap */
+  uint64_t scale_offset;      /* binary16 elements, % 4 == 0; request scale ranges must not overlap */
+} pkv_checkpoint_request_t;
+
+/* Validate a checkpoint write and build its plan on the current HIP device
+ * (same model constraints as pkv_restore_plan, plus num_kv_heads * head_dim
+ * / 16 * ceil(block_tokens / 4) <= 1024).  Every row of every block must sit
+ * on a mapped, in-range page (PKV_ERR_PAGE_UNMAPPED / _OUT_OF_RANGE);
+ * overlapping payload or scale ranges of two requests are
+ * PKV_ERR_INVALID_ARGUMENT.  Host arrays are copied.  Errors: as
+ * pkv_restore_plan. */
+pkv_status_t pkv_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoint_request_t* requests,
+                                 int32_t num_requests, pkv_plan_t** out);
+
+/* Enqueue the checkpoint write of a pkv_checkpoint_plan on `hip_stream`.
+ *   k_cache / v_cache : device, read only, cache_bytes each, 16-byte aligned;
+ *   payload / scales  : device outputs, >= the plan's payload_bytes / scale_bytes,
+ *                       16- / 8-byte aligned, not overlapping each other or the caches.
+ * Only bytes inside the requests' checkpoint ranges are written.
+ * A restore plan passed here (or a checkpoint plan passed to pkv_restore) is
+ * PKV_ERR_INVALID_ARGUMENT.  Errors: PKV_ERR_INVALID_ARGUMENT, PKV_ERR_DEVICE. */
+pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, const void* v_cache,
+                                 uint64_t cache_bytes, void* payload, uint64_t payload_bytes, void* scales,
+                                 uint64_t scale_bytes, void* hip_stream);
+
 /* What a plan reads and writes (for sizing buffers and for bandwidth
- * accounting). */
+ * accounting).  For a checkpoint plan, bytes_read counts cache rows read and
+ * bytes_written the payload and scale bytes written; restored_rows counts the
+ * suffix rows encoded per cache. */
 typedef struct {
   int64_t num_requests;
   int64_t num_units;          /* (request, layer, reused block) work units = workgroups launched */
@@ -169,7 +222,7 @@ typedef struct {
   uint64_t bytes_read;        /* payload + scale bytes of reused blocks (what the restore must read) */
   uint64_t bytes_written;     /* output bytes, K and V */
   int32_t device;             /* HIP device the plan lives on */
-  int32_t reserved;
+  int32_t kind;               /* 0 = restore plan, 1 = checkpoint plan */
 } pkv_plan_info_t;
 
 pkv_status_t pkv_plan_query(const pkv_plan_t* plan, pkv_plan_info_t* info);

@@ -98,13 +98,14 @@ def cache_values(bits: np.ndarray, cache_dtype: int) -> np.ndarray:
 # --------------------------------------------------------------------------
 
 def source_slots(shape, req, block: int) -> np.ndarray:
-    """Old-cache slot of every valid token of a block."""
+    """Old-cache slot of every valid token of a block (``req.src_row0`` and
+    the old context's page table ``req.src_page_table``)."""
     B, P = shape.block_tokens, shape.page_size
     n = min(B, req.suffix_tokens - block * B)
     slots = np.empty(n, dtype=np.int64)
     for t in range(n):
         row = req.src_row0 + block * B + t
-        page = int(req.page_table[row // P])
+        page = int(req.src_page_table[row // P])
         if page < 0 or page >= shape.pool_pages:
             raise ValueError("source row on an unmapped or out-of-range page")
         slots[t] = page * P + row % P
@@ -118,9 +119,10 @@ def source_slots(shape, req, block: int) -> np.ndarray:
 def quantize_tile(x: np.ndarray, bits: int) -> Tuple[np.ndarray, int, int]:
     """(codes uint8 [n, D], scale bits, zero bits) of one head's tile."""
     qmax = (1 << bits) - 1
-    zero_bits = int(f16_floor(np.array(x.min())))
+    # Signed zeros: a -0.0 extreme counts as +0.0 (adding +0.0 maps -0 to +0).
+    zero_bits = int(f16_floor(np.array(float(x.min()) + 0.0)))
     zero = float(_f16_values_from_bits(np.array(zero_bits)))
-    span = float(x.max()) - zero  # exact: both are short binary fractions
+    span = (float(x.max()) - zero) + 0.0  # exact: both are short binary fractions
     scale_bits = int(f16_ceil(np.array(span / qmax)))
     scale = float(_f16_values_from_bits(np.array(scale_bits)))
     if scale == 0.0:

@@ -25,7 +25,7 @@ PKV_ERR_DEVICE = -7
 
 # Every symbol include/pkv.h declares.
 EXPORTED = ("pkv_payload_size", "pkv_restore_plan", "pkv_restore", "pkv_free", "pkv_plan_query",
-            "pkv_status_string")
+            "pkv_status_string", "pkv_checkpoint_plan", "pkv_quantize_gather")
 
 
 class PkvModel(ctypes.Structure):
@@ -41,11 +41,17 @@ class PkvRequest(ctypes.Structure):
                 ("payload_offset", ctypes.c_uint64), ("scale_offset", ctypes.c_uint64)]
 
 
+class PkvCheckpointRequest(ctypes.Structure):
+    _fields_ = [("suffix_tokens", ctypes.c_int32), ("reserved", ctypes.c_int32), ("src_row0", ctypes.c_int64),
+                ("tags", ctypes.c_void_p), ("page_table", ctypes.c_void_p), ("num_logical_pages", ctypes.c_int32),
+                ("reserved2", ctypes.c_int32), ("payload_offset", ctypes.c_uint64), ("scale_offset", ctypes.c_uint64)]
+
+
 class PkvPlanInfo(ctypes.Structure):
     _fields_ = [("num_requests", ctypes.c_int64), ("num_units", ctypes.c_int64), ("restored_rows", ctypes.c_int64),
                 ("payload_bytes", ctypes.c_uint64), ("scale_bytes", ctypes.c_uint64),
                 ("cache_bytes", ctypes.c_uint64), ("bytes_read", ctypes.c_uint64),
-                ("bytes_written", ctypes.c_uint64), ("device", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("bytes_written", ctypes.c_uint64), ("device", ctypes.c_int32), ("kind", ctypes.c_int32)]
 
 
 class PkvError(RuntimeError):
@@ -79,6 +85,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pkv_plan_query.restype = i32
     lib.pkv_status_string.argtypes = [i32]
     lib.pkv_status_string.restype = ctypes.c_char_p
+    lib.pkv_checkpoint_plan.argtypes = [ctypes.POINTER(PkvModel), ctypes.POINTER(PkvCheckpointRequest), i32,
+                                        ctypes.POINTER(vp)]
+    lib.pkv_checkpoint_plan.restype = i32
+    lib.pkv_quantize_gather.argtypes = [vp, vp, vp, u64, vp, u64, vp, u64, vp]
+    lib.pkv_quantize_gather.restype = i32
     _lib = lib
     return lib
 
@@ -110,6 +121,68 @@ class _Requests:
                                        rep.ctypes.data if rep.size else None,
                                        pt.ctypes.data if pt.size else None, int(pt.size),
                                        int(getattr(r, "reserved", 0)), int(r.payload_offset), int(r.scale_offset))
+
+
+class _CheckpointRequests:
+    """A ctypes array of PkvCheckpointRequest plus the host arrays it points into.
+    Request objects need suffix_tokens, src_row0, tags, src_page_table (or
+    page_table), payload_offset and scale_offset."""
+
+    def __init__(self, requests: Sequence):
+        self.keep: List[np.ndarray] = []
+        self.array = (PkvCheckpointRequest * max(1, len(requests)))()
+        self.count = len(requests)
+        for i, r in enumerate(requests):
+            tags = np.ascontiguousarray(r.tags, dtype=np.uint8)
+            pt = np.ascontiguousarray(getattr(r, "src_page_table", None) if getattr(r, "src_page_table", None)
+                                      is not None else r.page_table, dtype=np.int32)
+            self.keep += [tags, pt]
+            self.array[i] = PkvCheckpointRequest(int(r.suffix_tokens), int(getattr(r, "reserved", 0)),
+                                                 int(r.src_row0), tags.ctypes.data if tags.size else None,
+                                                 pt.ctypes.data if pt.size else None, int(pt.size),
+                                                 int(getattr(r, "reserved2", 0)), int(r.payload_offset),
+                                                 int(r.scale_offset))
+
+
+def pkv_checkpoint_plan_status(shape, requests: Sequence) -> int:
+    lib = load()
+    m = make_model(shape)
+    reqs = _CheckpointRequests(requests)
+    out = ctypes.c_void_p()
+    st = lib.pkv_checkpoint_plan(ctypes.byref(m), reqs.array, reqs.count, ctypes.byref(out))
+    if out.value:
+        lib.pkv_free(out.value)
+    return st
+
+
+def pkv_checkpoint_plan(shape, requests: Sequence) -> "Plan":
+    lib = load()
+    m = make_model(shape)
+    reqs = _CheckpointRequests(requests)
+    out = ctypes.c_void_p()
+    st = lib.pkv_checkpoint_plan(ctypes.byref(m), reqs.array, reqs.count, ctypes.byref(out))
+    if st != PKV_OK:
+        raise PkvError(st, "pkv_checkpoint_plan")
+    return Plan(out.value)
+
+
+def pkv_quantize_gather(plan: "Plan", k_cache: int, v_cache: int, cache_bytes: int, payload: int,
+                        payload_bytes: int, scales: int, scale_bytes: int, stream: int = 0) -> None:
+    st = load().pkv_quantize_gather(plan.handle, k_cache, v_cache, cache_bytes, payload, payload_bytes, scales,
+                                    scale_bytes, stream or None)
+    if st != PKV_OK:
+        raise PkvError(st, "pkv_quantize_gather")
+
+
+def quantize_gather_tensors(plan: "Plan", k_cache, v_cache, payload, scales, stream=None) -> None:
+    """Marshal torch device tensors (contiguous) and the current stream into pkv_quantize_gather."""
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream(k_cache.device)
+    nbytes = lambda t: t.numel() * t.element_size()
+    pkv_quantize_gather(plan, k_cache.data_ptr(), v_cache.data_ptr(), nbytes(k_cache), payload.data_ptr(),
+                        nbytes(payload), scales.data_ptr(), nbytes(scales), stream.cuda_stream)
 
 
 def pkv_payload_size(shape, request):

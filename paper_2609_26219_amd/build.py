@@ -37,11 +37,14 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     cxx = shutil.which("g++") or "g++"
     plan_o = os.path.join(BUILD, "plan.o")
-    kern_o = os.path.join(BUILD, "restore.o")
     _run([cxx, *CXX_FLAGS, "-c", os.path.join(CSRC, "plan.cpp"), "-o", plan_o], verbose)
-    _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, "restore.hip"), "-o", kern_o], verbose)
+    objs = [plan_o]
+    for src in ("restore.hip", "gather.hip"):
+        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        objs.append(obj)
     tmp = LIB + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", plan_o, kern_o, "-o", tmp], verbose)
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -47,6 +47,8 @@ struct ReqInfo {
 
 // Everything the plan needs on the device, built on the host.
 struct HostPlan {
+  int32_t kind = 0;  // 0 = restore, 1 = checkpoint write
+  int32_t workgroup = kWorkgroup;
   pkv_model_t model;
   std::vector<Unit> units;
   std::vector<ReqInfo> reqs;
@@ -59,6 +61,30 @@ struct HostPlan {
 // Validate and build the host side of a plan.  Makes no HIP call.
 pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
                              HostPlan* out);
+
+// Same for a checkpoint write (quantize-and-gather).
+pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoint_request_t* requests,
+                                   int32_t num_requests, HostPlan* out);
+
+// Threads per workgroup of the checkpoint kernel: enough that each thread
+// holds at most kGatherTokens tokens of a block; 0 if the model needs more
+// than 1024.
+constexpr int kGatherTokens = 4;
+int32_t gather_workgroup(const pkv_model_t& m);
+
+// The plan object behind pkv_plan_t (host metadata + one device allocation).
+}  // namespace pkv
+struct pkv_plan {
+  pkv::HostPlan host;  // units, tables and page tables are dropped after upload
+  void* device_mem = nullptr;
+  pkv::Unit* d_units = nullptr;
+  double* d_tables = nullptr;
+  int32_t* d_page_tables = nullptr;
+  int device = -1;
+};
+namespace pkv {
+// Copy a built host plan to device memory on the current device and wrap it.
+pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out);
 
 // Bytes of one layer of a request's checkpoint (tags already validated).
 uint64_t layer_payload_bytes(const pkv_model_t& m, const uint8_t* tags, int64_t nb);

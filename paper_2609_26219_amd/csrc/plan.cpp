@@ -204,6 +204,123 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
   return PKV_OK;
 }
 
+int32_t gather_workgroup(const pkv_model_t& m) {
+  const int64_t cols = int64_t(m.num_kv_heads) * m.head_dim / 16;
+  const int64_t rows = (m.block_tokens + kGatherTokens - 1) / kGatherTokens;
+  const int64_t threads = (cols * rows + 63) / 64 * 64;
+  return threads <= 1024 ? int32_t(threads) : 0;
+}
+
+pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoint_request_t* requests,
+                                   int32_t num_requests, HostPlan* out) {
+  pkv_status_t st = check_model(model);
+  if (st != PKV_OK) return st;
+  if (num_requests < 0 || (num_requests > 0 && !requests) || !out) return PKV_ERR_INVALID_ARGUMENT;
+  const pkv_model_t& m = *model;
+  if (gather_workgroup(m) == 0) return PKV_ERR_INVALID_ARGUMENT;
+  const int64_t B = m.block_tokens, H = m.num_kv_heads, D = m.head_dim, P = m.page_size, L = m.num_layers;
+  const int lp2 = ilog2(P);
+  // Fields and tags.
+  for (int32_t r = 0; r < num_requests; ++r) {
+    const pkv_checkpoint_request_t& q = requests[r];
+    if (q.reserved != 0 || q.reserved2 != 0) return PKV_ERR_INVALID_ARGUMENT;
+    if (q.suffix_tokens < 0 || q.num_logical_pages < 0 || q.src_row0 < 0 || q.src_row0 > (int64_t(1) << 50))
+      return PKV_ERR_INVALID_ARGUMENT;
+    if (q.suffix_tokens > 0 && !q.tags) return PKV_ERR_INVALID_ARGUMENT;
+    if (q.num_logical_pages > 0 && !q.page_table) return PKV_ERR_INVALID_ARGUMENT;
+    if (q.payload_offset % 16 != 0 || q.scale_offset % 4 != 0) return PKV_ERR_INVALID_ARGUMENT;
+    if (q.payload_offset > (uint64_t(1) << 56) || q.scale_offset > (uint64_t(1) << 56)) return PKV_ERR_INVALID_ARGUMENT;
+    const int64_t nb = ceil_div(q.suffix_tokens, B);
+    for (int64_t b = 0; b < nb; ++b)
+      if (q.tags[b] > PKV_TAG_K4V4) return PKV_ERR_BAD_TAG;
+  }
+  // Every source row on a mapped, in-range page.
+  for (int32_t r = 0; r < num_requests; ++r) {
+    const pkv_checkpoint_request_t& q = requests[r];
+    if (q.suffix_tokens == 0) continue;
+    const int64_t first = q.src_row0 >> lp2, last = (q.src_row0 + q.suffix_tokens - 1) >> lp2;
+    for (int64_t lp = first; lp <= last; ++lp) {
+      if (lp >= q.num_logical_pages) return PKV_ERR_PAGE_OUT_OF_RANGE;
+      const int32_t pp = q.page_table[lp];
+      if (pp == -1) return PKV_ERR_PAGE_UNMAPPED;
+      if (pp < -1 || pp >= m.pool_pages) return PKV_ERR_PAGE_OUT_OF_RANGE;
+    }
+  }
+  // Output ranges of different requests must not overlap.
+  std::vector<std::pair<uint64_t, uint64_t>> pr, sr;
+  for (int32_t r = 0; r < num_requests; ++r) {
+    const pkv_checkpoint_request_t& q = requests[r];
+    const int64_t nb = ceil_div(q.suffix_tokens, B);
+    if (nb == 0) continue;
+    pr.emplace_back(q.payload_offset, q.payload_offset + uint64_t(L) * layer_payload_bytes(m, q.tags, nb));
+    sr.emplace_back(q.scale_offset, q.scale_offset + uint64_t(L) * nb * H * 4);
+  }
+  for (auto* v : {&pr, &sr}) {
+    std::sort(v->begin(), v->end());
+    for (size_t i = 1; i < v->size(); ++i)
+      if ((*v)[i].first < (*v)[i - 1].second) return PKV_ERR_INVALID_ARGUMENT;
+  }
+
+  HostPlan& hp = *out;
+  hp.kind = 1;
+  hp.workgroup = gather_workgroup(m);
+  hp.model = m;
+  hp.log2_page = lp2;
+  hp.units.clear();
+  hp.reqs.clear();
+  hp.tables.clear();
+  hp.page_tables.clear();
+  memset(&hp.info, 0, sizeof(hp.info));
+  hp.info.num_requests = num_requests;
+  hp.info.kind = 1;
+  hp.info.cache_bytes = uint64_t(L) * uint64_t(m.pool_pages) * uint64_t(P) * uint64_t(H) * uint64_t(D) * 2;
+  try {
+    for (int32_t r = 0; r < num_requests; ++r) {
+      const pkv_checkpoint_request_t& q = requests[r];
+      const int64_t nb = ceil_div(q.suffix_tokens, B);
+      const int64_t pt_off = int64_t(hp.page_tables.size());
+      hp.page_tables.insert(hp.page_tables.end(), q.page_table, q.page_table + q.num_logical_pages);
+      if (nb == 0) continue;
+      std::vector<uint64_t> block_off(nb);
+      uint64_t pos = 0;
+      for (int tag = 0; tag < 4; ++tag)
+        for (int64_t b = 0; b < nb; ++b)
+          if (q.tags[b] == tag) {
+            block_off[b] = pos;
+            pos += tile_bytes(m, kKeyBits[tag]) + tile_bytes(m, kValueBits[tag]);
+          }
+      const uint64_t layer_bytes = pos;
+      hp.info.payload_bytes = std::max<uint64_t>(hp.info.payload_bytes, q.payload_offset + uint64_t(L) * layer_bytes);
+      hp.info.scale_bytes = std::max<uint64_t>(hp.info.scale_bytes, (q.scale_offset + uint64_t(L) * nb * H * 4) * 2);
+      for (int64_t l = 0; l < L; ++l) {
+        for (int64_t b = 0; b < nb; ++b) {
+          const int tag = q.tags[b];
+          Unit u;
+          u.k_off = q.payload_offset + uint64_t(l) * layer_bytes + block_off[b];
+          u.v_off = u.k_off + tile_bytes(m, kKeyBits[tag]);
+          u.scale_off = q.scale_offset + (uint64_t(l) * nb + b) * H * 4;
+          u.row0 = q.src_row0 + b * B;
+          u.pt_off = pt_off;
+          u.table_off = 0;
+          u.layer = int32_t(l);
+          u.tag = tag;
+          u.n_valid = int32_t(std::min<int64_t>(B, q.suffix_tokens - b * B));
+          u.reserved = 0;
+          hp.units.push_back(u);
+        }
+        hp.info.bytes_written += layer_bytes + uint64_t(nb) * H * 4 * 2;
+      }
+      hp.info.restored_rows += int64_t(L) * q.suffix_tokens;
+    }
+  } catch (const std::bad_alloc&) {
+    return PKV_ERR_OUT_OF_MEMORY;
+  }
+  if (hp.units.size() > size_t(std::numeric_limits<int32_t>::max())) return PKV_ERR_INVALID_ARGUMENT;
+  hp.info.num_units = int64_t(hp.units.size());
+  hp.info.bytes_read = uint64_t(hp.info.restored_rows) * H * D * 2 * 2;
+  return PKV_OK;
+}
+
 }  // namespace pkv
 
 extern "C" {
@@ -231,6 +348,21 @@ pkv_status_t pkv_internal_host_units(const pkv_model_t* model, const pkv_request
   pkv_status_t st = pkv::build_host_plan(model, requests, num_requests, &hp);
   if (st != PKV_OK) return st;
   *count = int64_t(hp.units.size());
+  if (units_out && capacity >= *count && *count > 0)
+    memcpy(units_out, hp.units.data(), hp.units.size() * sizeof(pkv::Unit));
+  return PKV_OK;
+}
+
+// Internal test hook (not part of pkv.h): the work list of a checkpoint plan.
+pkv_status_t pkv_internal_checkpoint_units(const pkv_model_t* model, const pkv_checkpoint_request_t* requests,
+                                           int32_t num_requests, void* units_out, int64_t capacity, int64_t* count,
+                                           int32_t* workgroup) {
+  if (!count || !workgroup) return PKV_ERR_INVALID_ARGUMENT;
+  pkv::HostPlan hp;
+  pkv_status_t st = pkv::build_checkpoint_plan(model, requests, num_requests, &hp);
+  if (st != PKV_OK) return st;
+  *count = int64_t(hp.units.size());
+  *workgroup = hp.workgroup;
   if (units_out && capacity >= *count && *count > 0)
     memcpy(units_out, hp.units.data(), hp.units.size() * sizeof(pkv::Unit));
   return PKV_OK;

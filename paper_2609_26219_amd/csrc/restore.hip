@@ -271,31 +271,16 @@ bool ranges_overlap(const void* a, uint64_t na, const void* b, uint64_t nb) {
 }  // namespace
 }  // namespace pkv
 
-struct pkv_plan {
-  pkv::HostPlan host;  // units are dropped after upload; metadata kept
-  void* device_mem = nullptr;
-  pkv::Unit* d_units = nullptr;
-  double* d_tables = nullptr;
-  int32_t* d_page_tables = nullptr;
-  int device = -1;
-};
+namespace pkv {
 
-extern "C" {
-
-pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
-                              pkv_plan_t** out) {
-  if (!out) return PKV_ERR_INVALID_ARGUMENT;
+pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   *out = nullptr;
   pkv_plan* plan = new (std::nothrow) pkv_plan();
   if (!plan) return PKV_ERR_OUT_OF_MEMORY;
-  pkv_status_t st = pkv::build_host_plan(model, requests, num_requests, &plan->host);
-  if (st != PKV_OK) {
-    delete plan;
-    return st;
-  }
-  // Device side: one allocation, 256-byte aligned sections.
+  plan->host = std::move(hp);
+  // One allocation, 256-byte aligned sections.
   auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
-  const size_t n_units = plan->host.units.size() * sizeof(pkv::Unit);
+  const size_t n_units = plan->host.units.size() * sizeof(Unit);
   const size_t n_tab = plan->host.tables.size() * sizeof(double);
   const size_t n_pt = plan->host.page_tables.size() * sizeof(int32_t);
   const size_t total = al(n_units) + al(n_tab) + al(n_pt);
@@ -314,7 +299,7 @@ pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* req
       return e == hipErrorOutOfMemory ? PKV_ERR_OUT_OF_MEMORY : PKV_ERR_DEVICE;
     }
     char* p = static_cast<char*>(plan->device_mem);
-    plan->d_units = reinterpret_cast<pkv::Unit*>(p);
+    plan->d_units = reinterpret_cast<Unit*>(p);
     p += al(n_units);
     plan->d_tables = reinterpret_cast<double*>(p);
     p += al(n_tab);
@@ -331,16 +316,30 @@ pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* req
     }
   }
   // The device copy is authoritative; keep only the metadata on the host.
-  std::vector<pkv::Unit>().swap(plan->host.units);
+  std::vector<Unit>().swap(plan->host.units);
   std::vector<double>().swap(plan->host.tables);
   std::vector<int32_t>().swap(plan->host.page_tables);
   *out = plan;
   return PKV_OK;
 }
 
+}  // namespace pkv
+
+extern "C" {
+
+pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
+                              pkv_plan_t** out) {
+  if (!out) return PKV_ERR_INVALID_ARGUMENT;
+  *out = nullptr;
+  pkv::HostPlan hp;
+  const pkv_status_t st = pkv::build_host_plan(model, requests, num_requests, &hp);
+  if (st != PKV_OK) return st;
+  return pkv::upload_plan(std::move(hp), out);
+}
+
 pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t payload_bytes, const void* scales,
                          uint64_t scale_bytes, void* k_cache, void* v_cache, uint64_t cache_bytes, void* hip_stream) {
-  if (!plan) return PKV_ERR_INVALID_ARGUMENT;
+  if (!plan || plan->host.kind != 0) return PKV_ERR_INVALID_ARGUMENT;
   const pkv_plan_info_t& info = plan->host.info;
   if (info.num_units == 0) return PKV_OK;
   if (!payload || !scales || !k_cache || !v_cache) return PKV_ERR_INVALID_ARGUMENT;

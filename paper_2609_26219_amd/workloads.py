@@ -103,6 +103,9 @@ class Request:
     page_table: np.ndarray  # int32 [num_logical_pages], -1 = unmapped
     payload_offset: int = 0  # bytes
     scale_offset: int = 0  # fp16 elements
+    # The old context the checkpoint was written from (offload side):
+    src_row0: int = 0  # omega_0, old logical row of suffix token 0 (= dst_row0 - delta)
+    src_page_table: Optional[np.ndarray] = None  # int32, old context's logical -> physical pages
 
     @property
     def num_blocks(self) -> int:
@@ -320,10 +323,12 @@ class Case:
     outlier_pairs: int
     payload_nbytes: int = 0
     scale_elems: int = 0
+    src_pool_pages: int = 0  # pages per layer of the old context's caches
     _layer_cache: Dict[Tuple[int, int], Tuple[np.ndarray, np.ndarray]] = dataclasses.field(
         default_factory=dict, repr=False)
 
     def __post_init__(self):
+        self._assign_source_pages()
         off, soff = 0, 0
         for r in self.requests:
             r.payload_offset = off
@@ -333,6 +338,51 @@ class Case:
             soff += _round_up(se, 64)
         self.payload_nbytes = off
         self.scale_elems = soff
+
+    def _assign_source_pages(self) -> None:
+        """Old-context placement: omega_0 = rho_0 - delta, each request's old
+        logical pages on distinct random pages of a shared old pool (twice the
+        pages needed)."""
+        P = self.shape.page_size
+        need = []
+        for r in self.requests:
+            # Hand-built test cases may pick rho_0 < delta; their old rows start at 0.
+            r.src_row0 = max(0, int(r.dst_row0) - int(r.delta))
+            need.append(-(-(r.src_row0 + r.suffix_tokens) // P))
+        self.src_pool_pages = max(1, 2 * sum(need))
+        perm = _rng(self.seed, 7).permutation(self.src_pool_pages).astype(np.int32)
+        k = 0
+        for r, n in zip(self.requests, need):
+            r.src_page_table = perm[k:k + n].copy()
+            k += n
+
+    @property
+    def src_shape(self) -> Shape:
+        """Geometry of the old context's caches."""
+        return dataclasses.replace(self.shape, pool_pages=self.src_pool_pages)
+
+    def old_cache_layer(self, which: int, layer: int) -> np.ndarray:
+        """Bit patterns (cache dtype) of one layer of the old K (0) or V (1)
+        cache, ``[src_pool_pages, P, H, D]``: each request's suffix rows hold
+        its drawn values at their old slots; every other slot holds the
+        pre-fill pattern."""
+        s = self.src_shape
+        n = s.layer_elems
+        out = prefill_bits_np(np.arange(layer * n, (layer + 1) * n, dtype=np.int64), self.prefill_seed(2 + which))
+        flat = out.reshape(s.pool_slots, s.num_kv_heads, s.head_dim)
+        for ri, r in enumerate(self.requests):
+            k, v = self.raw_layer(ri, layer)
+            vals = (k if which == 0 else v)[:r.suffix_tokens]
+            rows = r.src_row0 + np.arange(r.suffix_tokens)
+            slots = r.src_page_table[rows // s.page_size].astype(np.int64) * s.page_size + rows % s.page_size
+            flat[slots] = to_cache_bits(vals, s.out_dtype)
+        return out.reshape(s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim)
+
+    def host_old_caches(self) -> Tuple[np.ndarray, np.ndarray]:
+        """Old K and V caches ``[L, src_pool_pages, P, H, D]`` (small cases)."""
+        L = self.shape.num_layers
+        return (np.stack([self.old_cache_layer(0, l) for l in range(L)]),
+                np.stack([self.old_cache_layer(1, l) for l in range(L)]))
 
     # -- raw draws and encoded layers ------------------------------------
     def source_layer(self, layer: int) -> int:
@@ -429,6 +479,17 @@ class Case:
         L = s.num_layers
         return {"payload_read": L * read, "scale_read": L * scales, "written": L * written,
                 "total": L * (read + scales + written)}
+
+
+def to_cache_bits(x: np.ndarray, out_dtype: int) -> np.ndarray:
+    """Bit patterns of float values stored in a fp16 or bf16 cache (the
+    libraries' own round-to-nearest-even conversions)."""
+    x = np.asarray(x, dtype=np.float32)
+    if out_dtype == OUT_FP16:
+        return x.astype(np.float16).view(np.uint16)
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(x)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
 
 
 def _encode_job(args):

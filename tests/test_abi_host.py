@@ -224,3 +224,65 @@ def test_empty_suffix_and_all_repair_are_valid():
     reqs[1].repair = np.ones_like(reqs[1].repair)
     reqs[1].page_table = np.full_like(reqs[1].page_table, -1)
     assert _status(shape, reqs) == VALID
+
+
+# ---------------------------------------------------------------------------
+# Checkpoint (quantize-and-gather) plan validation
+# ---------------------------------------------------------------------------
+
+def _ckpt_base():
+    case = wl.make_custom(8, L=2, H=2, D=64, B=16, P=16, n_tokens=(100, 40), deltas=(5, -3), rho0s=(20, 7))
+    return case.src_shape, [copy.copy(r) for r in case.requests]
+
+
+def _ck_status(shape, reqs):
+    return pb.pkv_checkpoint_plan_status(shape, reqs)
+
+
+def test_checkpoint_plan_valid_and_empty():
+    shape, reqs = _ckpt_base()
+    assert _ck_status(shape, reqs) == VALID
+    assert _ck_status(shape, []) == VALID
+
+
+def test_checkpoint_plan_errors():
+    shape, reqs = _ckpt_base()
+    r = copy.copy(reqs[0])
+    r.tags = r.tags.copy()
+    r.tags[0] = 5
+    assert _ck_status(shape, [r, reqs[1]]) == pb.PKV_ERR_BAD_TAG
+    r = copy.copy(reqs[0])
+    r.src_page_table = r.src_page_table.copy()
+    r.src_page_table[r.src_row0 // shape.page_size] = -1
+    assert _ck_status(shape, [r, reqs[1]]) == pb.PKV_ERR_PAGE_UNMAPPED
+    r.src_page_table[r.src_row0 // shape.page_size] = shape.pool_pages
+    assert _ck_status(shape, [r, reqs[1]]) == pb.PKV_ERR_PAGE_OUT_OF_RANGE
+    r = copy.copy(reqs[0])
+    r.src_page_table = r.src_page_table[:1].copy()
+    assert _ck_status(shape, [r, reqs[1]]) == pb.PKV_ERR_PAGE_OUT_OF_RANGE
+    r = copy.copy(reqs[1])
+    r.payload_offset = reqs[0].payload_offset + 16  # overlaps request 0's payload
+    assert _ck_status(shape, [reqs[0], r]) == pb.PKV_ERR_INVALID_ARGUMENT
+    r = copy.copy(reqs[1])
+    r.scale_offset = reqs[0].scale_offset + 4
+    assert _ck_status(shape, [reqs[0], r]) == pb.PKV_ERR_INVALID_ARGUMENT
+    for field, value in (("reserved", 1), ("reserved2", 1), ("payload_offset", 8), ("scale_offset", 2),
+                         ("src_row0", -1), ("suffix_tokens", -1)):
+        r = copy.copy(reqs[0])
+        setattr(r, field, value)
+        assert _ck_status(shape, [r, reqs[1]]) == pb.PKV_ERR_INVALID_ARGUMENT, field
+
+
+def test_checkpoint_plan_workgroup_limit():
+    import dataclasses
+    shape, reqs = _ckpt_base()
+    big = dataclasses.replace(shape, num_kv_heads=32, head_dim=128, block_tokens=32)  # 256 cols x 8 rows > 1024
+    for r in reqs:
+        nb = wl.num_blocks(r.suffix_tokens, 32)
+        r.tags = np.zeros(nb, np.uint8)
+    assert _ck_status(big, reqs) == pb.PKV_ERR_INVALID_ARGUMENT
+
+
+def test_plan_kinds_are_not_interchangeable(lib):
+    # without a GPU no plan can be built; the kind check itself is exercised on the GPU
+    assert lib.pkv_quantize_gather(None, None, None, 0, None, 0, None, 0, None) == pb.PKV_ERR_INVALID_ARGUMENT

@@ -1,0 +1,112 @@
+"""GPU parity of the checkpoint write (quantize-and-gather) against the CPU
+oracle, bit for bit, and of the full write -> restore cycle."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import quantize as oq
+from paper_2609_26219_amd import binding as pb
+from paper_2609_26219_amd import workloads as wl
+
+from parity import Stats, log
+
+pytestmark = pytest.mark.gpu
+
+FILL = 0xAB  # payload bytes outside every checkpoint range must keep this
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _t
+    if not _t.cuda.is_available():
+        pytest.skip("no GPU")
+    pb.load()
+    return _t
+
+
+def _gpu_checkpoint(case, torch):
+    s = case.src_shape
+    kc, vc = case.host_old_caches()
+    dk = torch.from_numpy(kc.view(np.int16)).cuda()
+    dv = torch.from_numpy(vc.view(np.int16)).cuda()
+    payload = torch.full((case.payload_nbytes,), FILL, dtype=torch.uint8, device="cuda")
+    scales = torch.full((case.scale_elems,), 0x5A5A, dtype=torch.int16, device="cuda")
+    plan = pb.pkv_checkpoint_plan(s, case.requests)
+    info = pb.pkv_plan_query(plan)
+    assert info["kind"] == 1
+    pb.quantize_gather_tensors(plan, dk, dv, payload, scales)
+    torch.cuda.synchronize()
+    return kc, vc, payload.cpu().numpy(), scales.cpu().numpy().view(np.uint16), info
+
+
+def _check_against_oracle(case, torch):
+    kc, vc, payload, scales, info = _gpu_checkpoint(case, torch)
+    ref_p, ref_s = oq.quantize_gather(case.src_shape, case.requests, kc, vc, case.payload_nbytes, case.scale_elems)
+    inside_p = np.zeros(case.payload_nbytes, bool)
+    inside_s = np.zeros(case.scale_elems, bool)
+    for r in case.requests:
+        pbytes, selems = wl.encoded_request_nbytes(case.shape, r)
+        inside_p[r.payload_offset: r.payload_offset + pbytes] = True
+        inside_s[r.scale_offset: r.scale_offset + selems] = True
+    bad = np.nonzero(payload[inside_p] != ref_p[inside_p])[0]
+    assert bad.size == 0, f"{bad.size} payload bytes differ, first at {bad[:5]}"
+    assert np.array_equal(scales[inside_s], ref_s[inside_s])
+    assert (payload[~inside_p] == FILL).all() and (scales[~inside_s] == 0x5A5A).all()
+    assert info["bytes_written"] == int(inside_p.sum()) + 2 * int(inside_s.sum())
+    return payload, scales, ref_p, ref_s
+
+
+@pytest.mark.parametrize("name,int4", [("tiny", wl.TAG_K8V4), ("tiny", wl.TAG_K4V4), ("llama8b_1l", wl.TAG_K8V4)])
+def test_checkpoint_bit_exact_named(name, int4, torch):
+    log(f"[gpu] checkpoint write {name}")
+    _check_against_oracle(wl.make_case(name, int4_tag=int4), torch)
+
+
+@pytest.mark.parametrize("params", [
+    dict(L=2, H=2, D=64, B=16, P=16, n_tokens=(100, 40), deltas=(5, -3), rho0s=(20, 7), out_dtype=wl.OUT_BF16),
+    dict(L=1, H=4, D=128, B=64, P=32, n_tokens=(130,), deltas=(9,), rho0s=(31,), out_dtype=wl.OUT_BF16),
+    dict(L=2, H=3, D=128, B=32, P=8, n_tokens=(70, 1, 33), deltas=(0, 2, -4), rho0s=(5, 9, 60), out_dtype=wl.OUT_FP16),
+    dict(L=1, H=8, D=256, B=8, P=16, n_tokens=(41,), deltas=(3,), rho0s=(5,), out_dtype=wl.OUT_BF16),
+], ids=["bf16_two_requests", "b64_bf16", "h3_three_requests_fp16", "d256_b8"])
+def test_checkpoint_bit_exact_custom(params, torch):
+    case = wl.make_custom(11, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), outlier_pairs=1, **params)
+    _check_against_oracle(case, torch)
+
+
+def test_write_then_restore_cycle(torch):
+    """Checkpoint written on the GPU, restored on the GPU into the new pages
+    with the key phase shift, compared element by element with the oracle's
+    restore of the oracle's own checkpoint."""
+    case = wl.make_case("llama8b_1l")
+    payload, scales, ref_p, ref_s = _check_against_oracle(case, torch)
+    s = case.shape
+    dpay = torch.from_numpy(payload).cuda()
+    dsc = torch.from_numpy(scales.view(np.int16)).cuda()
+    k = torch.zeros((s.num_layers, s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim), dtype=torch.int16,
+                    device="cuda")
+    v = torch.zeros_like(k)
+    plan = pb.pkv_restore_plan(s, case.requests)
+    pb.restore_tensors(plan, dpay, dsc, k, v)
+    torch.cuda.synchronize()
+    kh = k.cpu().numpy().view(np.uint16).reshape(s.num_layers, s.pool_slots, s.num_kv_heads, s.head_dim)
+    vh = v.cpu().numpy().view(np.uint16).reshape(kh.shape)
+    st = Stats()
+    req = case.requests[0]
+    layout = oracle.block_layout(req.tags, s.block_tokens, s.num_kv_heads, s.head_dim)
+    for b in oracle.reused_blocks(req):
+        slots, kk, vv = oracle.restore_block(ref_p, ref_s, s, req, 0, b, layout)  # oracle reads its own checkpoint
+        st.add(kh[0, slots], kk, s.out_dtype)
+        st.add(vh[0, slots], vv, s.out_dtype)
+    st.assert_ok(s.out_dtype)
+    log(f"  cycle: {st}")
+
+
+def test_plan_kinds_are_checked(torch):
+    case = wl.make_case("tiny")
+    ck = pb.pkv_checkpoint_plan(case.src_shape, case.requests)
+    rs = pb.pkv_restore_plan(case.shape, case.requests)
+    buf = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    p = buf.data_ptr()
+    assert pb.pkv_restore_status(ck, p, 1 << 16, p + (1 << 16), 1 << 16, p + (2 << 16), p + (3 << 16), 1 << 16,
+                                 0) == pb.PKV_ERR_INVALID_ARGUMENT
+    assert pb.load().pkv_quantize_gather(rs.handle, p, p, 0, p, 0, p, 0, None) == pb.PKV_ERR_INVALID_ARGUMENT

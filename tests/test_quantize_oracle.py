@@ -28,7 +28,7 @@ def test_hand_worked_checkpoint_write():
                 out_dtype=s["cache_dtype"])
     r = d["request"]
     req = _ns(suffix_tokens=r["suffix_tokens"], src_row0=r["src_row0"], tags=np.array(r["tags"], np.uint8),
-              page_table=np.array(r["page_table"], np.int32), payload_offset=0, scale_offset=0)
+              src_page_table=np.array(r["page_table"], np.int32), payload_offset=0, scale_offset=0)
     caches = []
     for kv in ("k", "v"):
         c = np.full((1, 3, 2, 1, 4), 0x7E00, dtype=np.uint16).reshape(1, 6, 1, 4)
@@ -108,7 +108,7 @@ def test_write_then_read_cycle_recovers_values():
                 out_dtype=oq.OUT_FP16, rope_theta=1e4)
     k = rng.standard_normal((L, pool, P, H, D)).astype(np.float16).view(np.uint16)
     v = rng.standard_normal((L, pool, P, H, D)).astype(np.float16).view(np.uint16)
-    src = _ns(suffix_tokens=N, src_row0=3, tags=tags, page_table=pt, payload_offset=0, scale_offset=0)
+    src = _ns(suffix_tokens=N, src_row0=3, tags=tags, src_page_table=pt, payload_offset=0, scale_offset=0)
     layer_bytes = sum(B * H * D * (oq.KEY_BITS[int(t)] + oq.VALUE_BITS[int(t)]) // 8 for t in tags)
     payload, scales = oq.quantize_gather(shape, [src], k, v, L * layer_bytes, L * nb * H * 4)
     dst = _ns(suffix_tokens=N, delta=0, dst_row0=3, tags=tags, repair=np.zeros(nb, np.uint8), page_table=pt,

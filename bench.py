@@ -3,7 +3,9 @@
 
 One step = one ``pkv_restore`` of the whole workload (every layer, every
 reused block) from a device-resident checkpoint into device-resident paged
-caches.  Prints one JSON line.
+caches.  Prints one JSON line.  The checkpoint itself is written on the GPU
+by ``pkv_quantize_gather`` from the drawn old caches; that write is timed too
+and reported under ``checkpoint_write``.
 
     python bench.py [--steps K] [--warmup W] [--workload llama8b_32l] [--int4 K8V4|K4V4]
 
@@ -30,6 +32,7 @@ sys.path.insert(0, ROOT)
 METRIC = "restored KV GB/s + % HBM peak; µs to restore 32K-token suffix (8B shape)"
 HBM_PEAK_GBPS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_26219_amd", "csrc", "restore.hip")
+GATHER_SRC = os.path.join(ROOT, "paper_2609_26219_amd", "csrc", "gather.hip")
 
 WORKLOAD_TEXT = {
     "llama8b_32l": "Llama-3-8B-shaped suffix restore: 32 layers x 8 KV heads x head_dim 128, 32768-token suffix, "
@@ -47,21 +50,21 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+def kernel_hash(src: str = KERNEL_SRC) -> str:
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str, int4: str):
+def measured_traffic(workload: str, int4: str, kernel: str = "restore_kernel", src: str = KERNEL_SRC):
     """HBM bytes per launch from the committed rocprofv3 PMC summary, if it was
     taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"restore_kernel_{workload}_{int4.lower()}_pmc.md")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_{int4.lower()}_pmc.md")
     if not os.path.exists(path):
         return None
     m = re.search(r"^traffic-json: (\{.*\})\s*$", open(path).read(), re.M)
     if not m:
         return None
     d = json.loads(m.group(1))
-    if d.get("kernel_sha256_16") != kernel_hash():
+    if d.get("kernel_sha256_16") != kernel_hash(src):
         return None
     return d.get("traffic_bytes_per_launch")
 
@@ -74,22 +77,28 @@ _CPU_CASE = None
 
 
 def _oracle_layer(args):
+    """One layer of one request: the oracle writes its checkpoint from the
+    drawn rows (timed separately), then restores it (timed)."""
     import dataclasses
 
     import numpy as np
 
     import oracle
+    from oracle import quantize as oq
 
     ri, layer = args
     case = _CPU_CASE
     req = case.requests[ri]
-    pb, sb = case.encoded_layer(ri, layer)
+    _, kb, vb = case.suffix_bits(ri, layer)
+    t = time.perf_counter()
+    pb, sb = oq.quantize_rows(case.shape, req, kb, vb)
+    t_write = time.perf_counter() - t
     one = dataclasses.replace(req, payload_offset=0, scale_offset=0)
     s1 = dataclasses.replace(case.shape, num_layers=1)
     cache = np.zeros((1, s1.pool_pages, s1.page_size, s1.num_kv_heads, s1.head_dim), np.uint16)
     t = time.perf_counter()
     oracle.restore(s1, [one], pb, sb.reshape(-1), cache, cache)
-    return time.perf_counter() - t
+    return time.perf_counter() - t, t_write
 
 
 def cpu_baseline(case, max_workers: int = 16, target_layers: int = 32):
@@ -104,10 +113,13 @@ def cpu_baseline(case, max_workers: int = 16, target_layers: int = 32):
     layers = list(range(min(case.shape.num_layers, max(target_layers, workers))))
     jobs = [(0, l) for l in layers]
     ctx = mp.get_context("fork")
-    t0 = time.perf_counter()
     with ctx.Pool(workers) as pool:
         per_layer = pool.map(_oracle_layer, jobs)
-    wall = time.perf_counter() - t0
+    # Each process times its own layer; the pool runs `workers` layers at once.
+    restore_cpu = sum(t for t, _ in per_layer)
+    write_cpu = sum(t for _, t in per_layer)
+    rounds = -(-len(layers) // workers)
+    wall = restore_cpu / len(layers) * rounds
     per_layer_bytes = case.algorithmic_bytes()["total"] / case.shape.num_layers
     sample_bytes = per_layer_bytes * len(layers)
     return {
@@ -116,12 +128,33 @@ def cpu_baseline(case, max_workers: int = 16, target_layers: int = 32):
         "cores": workers,
         "kind": "oracle",
         "sample": f"{len(layers)} of {case.shape.num_layers} layers of the same workload (request 0), one process "
-                  f"per layer, {workers} processes; wall {wall:.1f} s, cpu {sum(per_layer):.1f} s",
+                  f"per layer, {workers} processes; restore cpu {restore_cpu:.1f} s over {rounds} round(s) of "
+                  f"{workers} layers; checkpoint write (oracle quantize-and-gather) cpu {write_cpu:.1f} s, untimed "
+                  f"in value",
         "us_per_restore_extrapolated": round(wall / len(layers) * case.shape.num_layers * 1e6, 1),
+        "checkpoint_write_cpu_s_per_layer": round(write_cpu / len(layers), 3),
     }
 
 
 # ---------------------------------------------------------------------------
+
+
+def time_launches(torch, launch, n: int, warmup: int, stream):
+    """Per-launch durations (ms, sorted) from HIP events on ``stream`` and the
+    wall time (s) of the ``n`` timed launches."""
+    for i in range(warmup):
+        launch(i)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(n):
+        ev[i][0].record(stream)
+        launch(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return sorted(a.elapsed_time(b) for a, b in ev), wall
 
 
 def copy_reference(torch, nbytes: int = 4 << 30, reps: int = 10):
@@ -151,6 +184,7 @@ def main():
     ap.add_argument("--int4", default="K8V4", choices=["K8V4", "K4V4"],
                     help="representation of the int4 tag: K8V4 (the paper's tier) or uniform K4V4")
     ap.add_argument("--sets", type=int, default=2, help="buffer sets cycled between steps")
+    ap.add_argument("--write-steps", type=int, default=10, help="timed checkpoint-write launches")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ref", action="store_true")
     args = ap.parse_args()
@@ -164,7 +198,7 @@ def main():
 
     from paper_2609_26219_amd import binding
     from paper_2609_26219_amd import workloads as wl
-    from paper_2609_26219_amd.device import DeviceRestore
+    from paper_2609_26219_amd.device import DeviceCheckpoint, DeviceRestore, OldCaches
 
     binding.load()
     if not torch.cuda.is_available():
@@ -173,29 +207,32 @@ def main():
     int4_tag = wl.TAG_K8V4 if args.int4 == "K8V4" else wl.TAG_K4V4
     t = time.perf_counter()
     case = wl.make_case(args.workload, int4_tag=int4_tag)
-    case.warm()
-    log(f"[bench] generated {args.workload} in {time.perf_counter() - t:.1f} s")
-    sets = [DeviceRestore(case) for _ in range(max(1, args.sets))]
+    old = OldCaches(case)
+    log(f"[bench] drew {args.workload} old caches in {time.perf_counter() - t:.1f} s")
+    stream = torch.cuda.current_stream()
+
+    # Checkpoint write (offload side): every layer, every block, one launch.
+    ck = DeviceCheckpoint(case, old)
+    w_info = ck.info
+    w_bytes = w_info["bytes_read"] + w_info["bytes_written"]
+    w_ms, _ = time_launches(torch, lambda i: ck.write(stream), args.write_steps, 2, stream)
+    w_avg = sum(w_ms) / len(w_ms)
+    w_achieved = w_bytes / (w_avg * 1e-3) / 1e9
+    log(f"[bench] checkpoint write avg {w_avg * 1e3:.1f} us, {w_achieved:.0f} GB/s")
+    ck.old = None
+    del old
+    torch.cuda.empty_cache()
+
+    sets = [DeviceRestore(case, checkpoint=(ck.payload, ck.scales)) for _ in range(max(1, args.sets))]
+    del ck
+    torch.cuda.empty_cache()
     info = sets[0].info
     nbytes = info["bytes_read"] + info["bytes_written"]
     alg = case.algorithmic_bytes()
     assert nbytes == alg["total"], (nbytes, alg)
     log(f"[bench] {len(sets)} buffer set(s) ready; {info['num_units']} workgroups, {nbytes / 1e9:.3f} GB per step")
 
-    stream = torch.cuda.current_stream()
-    for i in range(args.warmup):
-        sets[i % len(sets)].run(stream)
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        ev[i][0].record(stream)
-        sets[i % len(sets)].run(stream)
-        ev[i][1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    kern_ms = sorted(a.elapsed_time(b) for a, b in ev)
+    kern_ms, wall = time_launches(torch, lambda i: sets[i % len(sets)].run(stream), args.steps, args.warmup, stream)
     kern_avg_ms = sum(kern_ms) / len(kern_ms)
     ms_per_step = wall * 1e3 / args.steps
     log(f"[bench] kernel avg {kern_avg_ms * 1e3:.1f} us (median {kern_ms[len(kern_ms) // 2] * 1e3:.1f}), "
@@ -239,6 +276,24 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": measured_traffic(args.workload, args.int4),
+        },
+        "checkpoint_write": {
+            "what": "pkv_quantize_gather of every block of every layer from the old paged caches "
+                    "(the offload side that produces the restored checkpoint), one launch",
+            "us": round(w_avg * 1e3, 1),
+            "us_p10_p50_p90": [round(w_ms[int(q * (len(w_ms) - 1))] * 1e3, 1) for q in (0.1, 0.5, 0.9)],
+            "launches": len(w_ms),
+            "algorithmic_bytes": w_bytes,
+            "bytes_read": w_info["bytes_read"],
+            "bytes_written": w_info["bytes_written"],
+            "roofline": {
+                "bound": "hbm",
+                "achieved": round(w_achieved, 1),
+                "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s",
+                "frac": round(w_achieved / HBM_PEAK_GBPS, 4),
+                "traffic": measured_traffic(args.workload, args.int4, "gather_kernel", GATHER_SRC),
+            },
         },
     }
     if not args.no_copy_ref:

@@ -161,6 +161,83 @@ def encode_tile(x: np.ndarray, n_valid: int, bits: int) -> Tuple[np.ndarray, np.
 # Steps 3-4: clustered layout
 # --------------------------------------------------------------------------
 
+def layer_layout_bytes(tags: Sequence[int], B: int, H: int, D: int) -> int:
+    return sum(B * H * D * (KEY_BITS[int(t)] + VALUE_BITS[int(t)]) // 8 for t in tags)
+
+
+def quantize_tiles_many(x: np.ndarray, n_valid: np.ndarray, bits: int) -> Tuple[np.ndarray, np.ndarray]:
+    """The per-tile definition of :func:`quantize_tile` applied to many tiles
+    at once: ``x`` fp64 ``[nb, B, H, D]``, rows ``>= n_valid[i]`` are padding.
+    Returns (codes uint8 [nb, B, H, D] with padding rows 0, bits [nb, H, 2] (scale, zero))."""
+    nb, B, H, D = x.shape
+    qmax = (1 << bits) - 1
+    valid = (np.arange(B)[None, :] < np.asarray(n_valid)[:, None])[:, :, None, None]
+    lo = np.where(valid, x, np.inf).min(axis=(1, 3)) + 0.0  # -0 counts as +0
+    hi = np.where(valid, x, -np.inf).max(axis=(1, 3))
+    zero_bits = f16_floor(lo)
+    zero = _f16_values_from_bits(zero_bits)
+    scale_bits = f16_ceil(((hi - zero) + 0.0) / qmax)
+    scale = _f16_values_from_bits(scale_bits)
+    safe = np.where(scale > 0, scale, 1.0)[:, None, :, None]
+    q = np.clip(np.rint((x - zero[:, None, :, None]) / safe), 0, qmax)
+    q = np.where((scale > 0)[:, None, :, None] & valid, q, 0)
+    return q.astype(np.uint8), np.stack([scale_bits, zero_bits], axis=-1)
+
+
+def gather_rows(shape, req, layer_cache: np.ndarray) -> np.ndarray:
+    """Step 1 for one layer: the request's suffix rows, in token order, from
+    one layer of an old cache (uint16 ``[pool_pages, P, H, D]``)."""
+    H, D = shape.num_kv_heads, shape.head_dim
+    flat = np.asarray(layer_cache, dtype=np.uint16).reshape(-1, H, D)
+    nb = len(req.tags)
+    if nb == 0:
+        return np.zeros((0, H, D), np.uint16)
+    return np.concatenate([flat[source_slots(shape, req, b)] for b in range(nb)])
+
+
+def quantize_rows(shape, req, k_rows: np.ndarray, v_rows: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Steps 2-4 for one layer of one request from its gathered suffix rows
+    (uint16 cache bit patterns ``[suffix_tokens, H, D]``): (payload bytes,
+    scale bits ``[NB, H, 2, 2]``)."""
+    B, H, D = shape.block_tokens, shape.num_kv_heads, shape.head_dim
+    nb = len(req.tags)
+    n_valid = np.minimum(B, req.suffix_tokens - np.arange(nb) * B)
+    scales = np.zeros((nb, H, 2, 2), dtype=np.uint16)
+    tiles = []
+    for rows in (k_rows, v_rows):
+        rows = np.asarray(rows, dtype=np.uint16).reshape(-1, H, D)
+        assert rows.shape[0] == req.suffix_tokens
+        x = np.zeros((nb * B, H, D), dtype=np.float64)
+        x[:req.suffix_tokens] = cache_values(rows, shape.out_dtype)
+        tiles.append(x.reshape(nb, B, H, D))
+    pieces = []
+    tags = np.asarray(req.tags)
+    for tag in (FP16, K8V8, K8V4, K4V4):
+        blocks = np.nonzero(tags == tag)[0]
+        if len(blocks) == 0:
+            continue
+        parts = []
+        for which, bits in ((0, KEY_BITS[tag]), (1, VALUE_BITS[tag])):
+            x = tiles[which][blocks]
+            if bits == 16:
+                h = x.astype(np.float16)
+                h[np.arange(B)[None, :] >= n_valid[blocks][:, None]] = 0
+                parts.append(h.view(np.uint8).reshape(len(blocks), -1))
+            else:
+                codes, sz = quantize_tiles_many(x, n_valid[blocks], bits)
+                scales[blocks, :, which, :] = sz
+                parts.append(pack_tile(codes, bits).reshape(len(blocks), -1))
+        pieces.append(np.concatenate(parts, axis=1).reshape(-1))  # K tile then V tile, per block
+    payload = np.concatenate(pieces) if pieces else np.zeros(0, np.uint8)
+    return payload, scales
+
+
+def quantize_layer(shape, req, k_layer: np.ndarray, v_layer: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """One layer of one request's checkpoint from that layer of the old caches
+    (uint16 ``[pool_pages, P, H, D]``): (payload bytes, scale bits ``[NB, H, 2, 2]``)."""
+    return quantize_rows(shape, req, gather_rows(shape, req, k_layer), gather_rows(shape, req, v_layer))
+
+
 def quantize_gather(shape, requests: Sequence, k_cache: np.ndarray, v_cache: np.ndarray,
                     payload_bytes: int, scale_elems: int) -> Tuple[np.ndarray, np.ndarray]:
     """Encode every block of every request from the caches (uint16 bit
@@ -170,15 +247,31 @@ def quantize_gather(shape, requests: Sequence, k_cache: np.ndarray, v_cache: np.
     L, B, H, D = shape.num_layers, shape.block_tokens, shape.num_kv_heads, shape.head_dim
     payload = np.zeros(payload_bytes, dtype=np.uint8)
     scales = np.zeros(scale_elems, dtype=np.uint16)
+    for req in requests:
+        nb = len(req.tags)
+        layer_bytes = layer_layout_bytes(req.tags, B, H, D)
+        for layer in range(L):
+            pb, sb = quantize_layer(shape, req, k_cache[layer], v_cache[layer])
+            o = req.payload_offset + layer * layer_bytes
+            payload[o:o + pb.size] = pb
+            so = req.scale_offset + layer * nb * H * 4
+            scales[so:so + sb.size] = sb.reshape(-1)
+    return payload, scales
+
+
+def quantize_gather_per_tile(shape, requests: Sequence, k_cache: np.ndarray, v_cache: np.ndarray,
+                             payload_bytes: int, scale_elems: int) -> Tuple[np.ndarray, np.ndarray]:
+    """The same result tile by tile with :func:`encode_tile` (slow; for small cases)."""
+    L, B, H, D = shape.num_layers, shape.block_tokens, shape.num_kv_heads, shape.head_dim
+    payload = np.zeros(payload_bytes, dtype=np.uint8)
+    scales = np.zeros(scale_elems, dtype=np.uint16)
     kf = np.asarray(k_cache, dtype=np.uint16).reshape(L, -1, H, D)
     vf = np.asarray(v_cache, dtype=np.uint16).reshape(L, -1, H, D)
     for req in requests:
         nb = len(req.tags)
-        # clustered order: FP16 run, K8V8 run, K8V4 run, K4V4 run
         order = [b for tag in (FP16, K8V8, K8V4, K4V4) for b in range(nb) if int(req.tags[b]) == tag]
         for layer in range(L):
-            pos = req.payload_offset + layer * sum(
-                B * H * D * (KEY_BITS[int(t)] + VALUE_BITS[int(t)]) // 8 for t in req.tags)
+            pos = req.payload_offset + layer * layer_layout_bytes(req.tags, B, H, D)
             for b in order:
                 tag = int(req.tags[b])
                 n = min(B, req.suffix_tokens - b * B)

@@ -1,13 +1,21 @@
-"""Device buffers for a restore: torch supplies memory and streams only.
+"""Device buffers for checkpoint writes and restores: torch supplies memory
+and streams only.
 
-``DeviceRestore`` uploads a generated checkpoint, pre-fills the two caches
-with a recomputable pattern, builds the plan through the C ABI and launches
-``pkv_restore`` on the current torch stream.  No restore arithmetic happens
-here.
+* :class:`OldCaches` places the drawn suffix rows of every request into the
+  old context's paged caches on the GPU (every other slot holds NaN).
+* :class:`DeviceCheckpoint` writes the checkpoint from them with
+  ``pkv_quantize_gather``.
+* :class:`DeviceRestore` holds a checkpoint and the destination caches
+  (pre-filled with a recomputable pattern), builds the restore plan and
+  launches ``pkv_restore`` on the current stream.
+
+No step of the method's arithmetic happens here.
 """
 from __future__ import annotations
 
-from typing import Optional
+import dataclasses
+import multiprocessing as mp
+from typing import Dict, Iterator, Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -22,45 +30,168 @@ def _to_int16(t):
     return torch.where(t >= 32768, t - 65536, t).to(torch.int16)
 
 
-class DeviceRestore:
+_DRAW_CASE = None
+
+
+def _draw_job(key):
+    ri, layer = key
+    return key, _DRAW_CASE.suffix_bits(ri, layer)
+
+
+def suffix_rows(case: wl.Case, layers: Sequence[int], workers: Optional[int] = None
+                ) -> Iterator[Tuple[int, int, Tuple[np.ndarray, np.ndarray, np.ndarray]]]:
+    """Yield (request, layer, (old slots, K bits, V bits)) for every layer in
+    ``layers`` (layer-major) and every request.  Each distinct draw is made
+    once, in worker processes, and dropped after its last use."""
+    global _DRAW_CASE
+    order = [(ri, layer) for layer in layers for ri in range(len(case.requests))]
+    keys = list(dict.fromkeys((ri, case.source_layer(l)) for ri, l in order))
+    last_use = {(ri, case.source_layer(l)): i for i, (ri, l) in enumerate(order)}
+    workers = min(workers or wl.default_workers(), len(keys))
+    pool = None
+    if workers > 1:
+        _DRAW_CASE = case
+        pool = mp.get_context("fork").Pool(workers)
+        results = pool.imap(_draw_job, keys)
+    else:
+        results = ((k, case.suffix_bits(*k)) for k in keys)
+    try:
+        drawn: Dict[Tuple[int, int], Tuple[np.ndarray, np.ndarray, np.ndarray]] = {}
+        for i, (ri, layer) in enumerate(order):
+            key = (ri, case.source_layer(layer))
+            while key not in drawn:
+                k, val = next(results)
+                drawn[k] = val
+            val = drawn[key]
+            if last_use[key] == i:
+                del drawn[key]
+            yield ri, layer, val
+    finally:
+        if pool is not None:
+            pool.terminate()
+            pool.join()
+
+
+def _scatter_rows(cache_layer, slots, bits):
+    import torch
+
+    s = cache_layer.shape
+    flat = cache_layer.view(-1, s[-2], s[-1])
+    idx = torch.from_numpy(slots).to(cache_layer.device)
+    flat.index_copy_(0, idx, torch.from_numpy(bits.view(np.int16)).to(cache_layer.device))
+
+
+class OldCaches:
+    """The old context's K and V caches on the device, all layers."""
+
     def __init__(self, case: wl.Case, device: str = "cuda", workers: Optional[int] = None):
+        import torch
+
+        self.case = case
+        s = case.src_shape
+        shape = (s.num_layers, s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim)
+        nan = wl.cache_nan_bits(s.out_dtype)
+        nan = nan - 65536 if nan >= 32768 else nan
+        self.k = torch.full(shape, nan, dtype=torch.int16, device=device)
+        self.v = torch.full(shape, nan, dtype=torch.int16, device=device)
+        for ri, layer, (slots, kb, vb) in suffix_rows(case, range(s.num_layers), workers):
+            _scatter_rows(self.k[layer], slots, kb)
+            _scatter_rows(self.v[layer], slots, vb)
+        torch.cuda.synchronize(device)
+
+
+def alloc_checkpoint(case: wl.Case, device: str = "cuda"):
+    """Zeroed payload (uint8) and scale (int16) device buffers of a case."""
+    import torch
+
+    payload = torch.zeros(max(16, case.payload_nbytes), dtype=torch.uint8, device=device)
+    scales = torch.zeros(max(4, case.scale_elems), dtype=torch.int16, device=device)
+    return payload, scales
+
+
+class DeviceCheckpoint:
+    """Checkpoint write of all layers from :class:`OldCaches` (one launch)."""
+
+    def __init__(self, case: wl.Case, old: OldCaches, device: str = "cuda"):
+        self.case = case
+        self.old = old
+        self.payload, self.scales = alloc_checkpoint(case, device)
+        self.plan = binding.pkv_checkpoint_plan(case.src_shape, case.requests)
+        self.info = binding.pkv_plan_query(self.plan)
+
+    def write(self, stream=None) -> None:
+        binding.quantize_gather_tensors(self.plan, self.old.k, self.old.v, self.payload, self.scales, stream)
+
+
+def write_checkpoint_layerwise(case: wl.Case, payload, scales, device: str = "cuda",
+                               workers: Optional[int] = None) -> None:
+    """Write a case's checkpoint on the GPU one layer at a time, through one
+    reusable old-cache layer (for cases whose old caches do not fit at once)."""
+    import torch
+
+    s1 = dataclasses.replace(case.src_shape, num_layers=1)
+    shape = (1, s1.pool_pages, s1.page_size, s1.num_kv_heads, s1.head_dim)
+    nan = wl.cache_nan_bits(s1.out_dtype)
+    nan = nan - 65536 if nan >= 32768 else nan
+    k = torch.empty(shape, dtype=torch.int16, device=device)
+    v = torch.empty(shape, dtype=torch.int16, device=device)
+    current = None
+    rows = []
+
+    def flush(layer):
+        k.fill_(nan)
+        v.fill_(nan)
+        for ri, (slots, kb, vb) in rows:
+            _scatter_rows(k[0], slots, kb)
+            _scatter_rows(v[0], slots, vb)
+        reqs = [dataclasses.replace(r, payload_offset=case.layer_payload_offset(ri, layer),
+                                    scale_offset=case.layer_scale_offset(ri, layer))
+                for ri, r in enumerate(case.requests)]
+        plan = binding.pkv_checkpoint_plan(s1, reqs)
+        binding.quantize_gather_tensors(plan, k, v, payload, scales)
+        torch.cuda.synchronize(device)
+        binding.pkv_free(plan)
+
+    for ri, layer, drawn in suffix_rows(case, range(case.shape.num_layers), workers):
+        if current is not None and layer != current:
+            flush(current)
+            rows = []
+        current = layer
+        rows.append((ri, drawn))
+    if current is not None:
+        flush(current)
+
+
+class DeviceRestore:
+    """A checkpoint and the destination caches of a case, with its restore plan.
+
+    ``checkpoint`` is ``None`` (write it on the GPU from the drawn old
+    caches), a pair of host arrays (payload uint8, scales uint16) to upload, or
+    a pair of device tensors to copy."""
+
+    def __init__(self, case: wl.Case, device: str = "cuda", checkpoint=None, workers: Optional[int] = None):
         import torch
 
         self.case = case
         self.device = torch.device(device)
         s = case.shape
-        case.warm(workers)
-        self.payload = torch.empty(max(16, case.payload_nbytes), dtype=torch.uint8, device=self.device)
-        self.scales = torch.empty(max(4, case.scale_elems), dtype=torch.int16, device=self.device)
-        self.scales.fill_(wl.FP16_NAN_BITS)
-        self._upload()
+        self.payload, self.scales = alloc_checkpoint(case, device)
+        if checkpoint is None:
+            write_checkpoint_layerwise(case, self.payload, self.scales, device, workers)
+        else:
+            p, sc = checkpoint
+            if isinstance(p, np.ndarray):
+                self.payload[:p.size].copy_(torch.from_numpy(p))
+                self.scales[:sc.size].copy_(torch.from_numpy(np.asarray(sc, np.uint16).view(np.int16)))
+            else:
+                self.payload.copy_(p)
+                self.scales.copy_(sc)
         cache_shape = (s.num_layers, s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim)
         self.k_cache = torch.empty(cache_shape, dtype=torch.int16, device=self.device)
         self.v_cache = torch.empty(cache_shape, dtype=torch.int16, device=self.device)
         self.prefill()
         self.plan = binding.pkv_restore_plan(s, case.requests)
         self.info = binding.pkv_plan_query(self.plan)
-
-    def _upload(self) -> None:
-        import torch
-
-        c = self.case
-        for ri, r in enumerate(c.requests):
-            first = {}
-            for layer in range(c.shape.num_layers):
-                pb, sb = c.encoded_layer(ri, layer)
-                o = c.layer_payload_offset(ri, layer)
-                so = c.layer_scale_offset(ri, layer)
-                src = c.source_layer(layer)
-                if src in first:  # repeated layer: device-to-device copy of its source
-                    fo, fso = first[src]
-                    self.payload[o:o + pb.size].copy_(self.payload[fo:fo + pb.size])
-                    self.scales[so:so + sb.size].copy_(self.scales[fso:fso + sb.size])
-                    continue
-                first[src] = (o, so)
-                self.payload[o:o + pb.size].copy_(torch.from_numpy(pb))
-                self.scales[so:so + sb.size].copy_(torch.from_numpy(sb.reshape(-1).view(np.int16)))
-        torch.cuda.synchronize(self.device)
 
     def prefill(self) -> None:
         """Fill both caches with the generator's position-dependent pattern."""

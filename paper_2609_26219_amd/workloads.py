@@ -1,30 +1,13 @@
 """Seeded synthetic suffix-restore workloads.
 
-This module is the one place where inputs are made, and both the CPU oracle
-(``oracle/``) and the GPU path (the ``libpkv`` binding) consume what it makes.
-It draws the random parts of a resume (per-block precision tags, the repair
-mask, page tables, the edit shift, key and value tensors) and encodes them
-into a checkpoint payload the way the offload side of PatchKV does
-(Section IV-D: gather block rows, compute per-block scales, pack FP16 / 8-bit /
-4-bit codes, cluster same-tag blocks into runs).
-
-It holds none of the restore's arithmetic: it never dequantizes, rotates or
-places a row.  The encoder it contains is the *inverse* direction (float ->
-codes), which the restore never performs.
-
-Checkpoint format written here (one request):
-
-* payload, per layer ``l`` in order, per tag in order FP16, K8V8, K8V4, K4V4,
-  per block ``b`` with that tag in ascending order (repair blocks included,
-  their bytes are poison): the block's K tile then its V tile.  A tile is the
-  block's ``B`` gathered cache rows, token-major ``[B][H][D]``, in the tag's
-  key (resp. value) format: FP16 = IEEE binary16, 8-bit = one u8 code per
-  channel, 4-bit = two codes per byte with channel ``2j`` in the low nibble of
-  byte ``j``.  Rows past the end of the suffix in the last block are padding
-  (code 0).
-* scales, fp16 ``[L][NB][H][2 (K, V)][2 (scale, zero)]``; a quantized channel
-  decodes as ``code * scale + zero``.  Entries of FP16 tiles and of repair
-  blocks are NaN.
+This module is the one place where inputs are drawn; the CPU oracle
+(``oracle/``), the tests and the benchmark consume what it draws.  It holds
+none of the method's arithmetic: it draws the random parts of an edit and
+resume (per-block precision tags, the repair mask, old and new page tables,
+the edit shift, key and value tensors) and places the drawn values in the old
+context's paged cache.  Checkpoints are written from those caches by the
+quantize-and-gather step itself (the oracle's on the host, libpkv's on the
+GPU); nothing here quantizes, dequantizes, rotates or places a restored row.
 
 Value model (synthetic stand-in for the paper's long-context models, whose
 weights and QA datasets are not available here): stored keys and values are
@@ -33,13 +16,16 @@ outliers scaled by 8.  Because the outlier scale is applied to both channels
 of a rotary pair, each pair stays an isotropic Gaussian, so a key rotated to
 any old position has the same distribution as the pre-rotation key and the
 stored (post-rotation) keys can be drawn directly.
+
+Checkpoint sizes follow the format of ``include/pkv.h``: per layer, per tag,
+per block a K tile and a V tile of B rows x H heads x D channels at 16, 8 or
+4 bits per channel.
 """
 from __future__ import annotations
 
 import dataclasses
 import math
 import os
-from concurrent.futures import ProcessPoolExecutor
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -51,7 +37,6 @@ VALUE_BITS = (16, 8, 4, 4)
 OUT_FP16, OUT_BF16 = 0, 1
 
 FP16_NAN_BITS = 0x7E00
-POISON_CODE = 0xFF
 
 # Seed streams (spawn keys) so every piece can be regenerated in isolation.
 _STREAM_TAGS, _STREAM_REPAIR, _STREAM_PAGES, _STREAM_POS, _STREAM_K, _STREAM_V = range(6)
@@ -134,79 +119,8 @@ def encoded_request_nbytes(shape: Shape, req: Request) -> Tuple[int, int]:
 
 
 # ----------------------------------------------------------------------------
-# Encoder (offload direction: floats -> codes).  Not part of the restore.
+# Draws
 # ----------------------------------------------------------------------------
-
-def fp16_round_down(x: np.ndarray) -> np.ndarray:
-    """Largest binary16 value <= x (x finite, float64)."""
-    h = x.astype(np.float16)
-    too_big = h.astype(np.float64) > x
-    h[too_big] = np.nextafter(h[too_big], np.float16(-np.inf))
-    return h
-
-
-def fp16_round_up(x: np.ndarray) -> np.ndarray:
-    """Smallest binary16 value >= x (x finite, float64)."""
-    h = x.astype(np.float16)
-    too_small = h.astype(np.float64) < x
-    h[too_small] = np.nextafter(h[too_small], np.float16(np.inf))
-    return h
-
-
-def quantize_tiles(x: np.ndarray, n_valid: np.ndarray, bits: int):
-    """Asymmetric per-(block, head) quantizer.
-
-    ``x`` is float32 ``[nb, B, H, D]``; rows ``>= n_valid[i]`` of block ``i``
-    are padding and excluded from the range.  Zero = min rounded down to fp16,
-    scale = (max - zero) / (2^bits - 1) rounded up to fp16, code =
-    rint((x - zero) / scale) in double precision, clipped to the code range
-    (a zero scale means every valid element equals the zero: code 0).  The
-    rounding directions keep every element within half a step of its decoded
-    value.  Returns (codes uint8 [nb,B,H,D], scale fp16 [nb,H], zero fp16 [nb,H]).
-    """
-    nb, B, H, D = x.shape
-    qmax = (1 << bits) - 1
-    n_valid = np.asarray(n_valid)
-    lo = x.min(axis=(1, 3)).astype(np.float64)
-    hi = x.max(axis=(1, 3)).astype(np.float64)
-    for i in np.nonzero(n_valid < B)[0]:  # partial block: range over valid rows only
-        lo[i] = x[i, :n_valid[i]].min(axis=(0, 2))
-        hi[i] = x[i, :n_valid[i]].max(axis=(0, 2))
-    zero = fp16_round_down(lo)
-    scale = fp16_round_up((hi - zero.astype(np.float64)) / qmax)
-    s64 = scale.astype(np.float64)
-    s64[s64 == 0] = 1.0
-    q = x.astype(np.float64)
-    q -= zero.astype(np.float64)[:, None, :, None]
-    q /= s64[:, None, :, None]
-    np.rint(q, out=q)
-    np.clip(q, 0, qmax, out=q)
-    codes = q.astype(np.uint8)
-    for i in np.nonzero(n_valid < B)[0]:
-        codes[i, n_valid[i]:] = 0
-    return codes, scale, zero
-
-
-def pack_nibbles(codes: np.ndarray) -> np.ndarray:
-    """Two 4-bit codes per byte along the last axis; channel 2j -> low nibble."""
-    c = codes.reshape(codes.shape[:-1] + (codes.shape[-1] // 2, 2))
-    return (c[..., 0] | (c[..., 1] << 4)).astype(np.uint8)
-
-
-def _encode_tiles(x: np.ndarray, n_valid: np.ndarray, bits: int):
-    """Encode ``[nb, B, H, D]`` float32 tiles; returns (bytes [nb, tile_bytes], scale, zero)."""
-    nb = x.shape[0]
-    if bits == 16:
-        h = x.astype(np.float16)
-        pad = np.arange(x.shape[1])[None, :] >= n_valid[:, None]
-        h[pad] = np.float16(0)
-        nanf = np.full((nb, x.shape[2]), np.nan, dtype=np.float16)
-        return h.view(np.uint8).reshape(nb, -1), nanf, nanf
-    codes, s, z = quantize_tiles(x, n_valid, bits)
-    if bits == 4:
-        codes = pack_nibbles(codes)
-    return codes.reshape(nb, -1), s, z
-
 
 def draw_layer(shape: Shape, seed: int, req_index: int, layer: int, n_tokens: int,
                outlier_pairs: int) -> Tuple[np.ndarray, np.ndarray]:
@@ -228,46 +142,6 @@ def draw_layer(shape: Shape, seed: int, req_index: int, layer: int, n_tokens: in
     k[n_tokens:] = 0
     v[n_tokens:] = 0
     return k, v
-
-
-def encode_layer(shape: Shape, req: Request, k: np.ndarray, v: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
-    """Encode one layer of one request into (payload bytes, fp16 scale bits [NB, H, 2, 2])."""
-    B, H, D = shape.block_tokens, shape.num_kv_heads, shape.head_dim
-    NB = req.num_blocks
-    N = req.suffix_tokens
-    kt = k.reshape(NB, B, H, D)
-    vt = v.reshape(NB, B, H, D)
-    n_valid = np.minimum(B, N - np.arange(NB) * B).astype(np.int64)
-    scales = np.full((NB, H, 2, 2), np.nan, dtype=np.float16)
-    pieces: List[np.ndarray] = []
-    repair = np.asarray(req.repair) != 0
-    for tag in range(4):
-        blocks = np.nonzero(np.asarray(req.tags) == tag)[0]
-        if len(blocks) == 0:
-            continue
-        kb, ks, kz = _encode_tiles(kt[blocks], n_valid[blocks], KEY_BITS[tag])
-        vb, vs, vz = _encode_tiles(vt[blocks], n_valid[blocks], VALUE_BITS[tag])
-        rep = repair[blocks]
-        if rep.any():  # repair blocks are never read by a restore: poison them
-            poison_k = FP16_NAN_BITS if KEY_BITS[tag] == 16 else POISON_CODE
-            poison_v = FP16_NAN_BITS if VALUE_BITS[tag] == 16 else POISON_CODE
-            kb[rep] = _poison_bytes(kb.shape[1], poison_k, KEY_BITS[tag])
-            vb[rep] = _poison_bytes(vb.shape[1], poison_v, VALUE_BITS[tag])
-        if tag != TAG_FP16:
-            scales[blocks, :, 0, 0] = ks
-            scales[blocks, :, 0, 1] = kz
-            scales[blocks, :, 1, 0] = vs
-            scales[blocks, :, 1, 1] = vz
-        scales[blocks[rep]] = np.float16(np.nan)
-        pieces.append(np.concatenate([kb, vb], axis=1).reshape(-1))
-    payload = np.concatenate(pieces) if pieces else np.zeros(0, np.uint8)
-    return payload, scales.view(np.uint16)
-
-
-def _poison_bytes(nbytes: int, pattern: int, bits: int) -> np.ndarray:
-    if bits == 16:
-        return np.full(nbytes // 2, pattern, dtype=np.uint16).view(np.uint8)
-    return np.full(nbytes, pattern, dtype=np.uint8)
 
 
 def _rng(seed: int, *key: int) -> np.random.Generator:
@@ -324,8 +198,6 @@ class Case:
     payload_nbytes: int = 0
     scale_elems: int = 0
     src_pool_pages: int = 0  # pages per layer of the old context's caches
-    _layer_cache: Dict[Tuple[int, int], Tuple[np.ndarray, np.ndarray]] = dataclasses.field(
-        default_factory=dict, repr=False)
 
     def __post_init__(self):
         self._assign_source_pages()
@@ -364,19 +236,14 @@ class Case:
     def old_cache_layer(self, which: int, layer: int) -> np.ndarray:
         """Bit patterns (cache dtype) of one layer of the old K (0) or V (1)
         cache, ``[src_pool_pages, P, H, D]``: each request's suffix rows hold
-        its drawn values at their old slots; every other slot holds the
-        pre-fill pattern."""
+        its drawn values at their old slots; every other slot holds NaN, so a
+        read of a wrong slot shows."""
         s = self.src_shape
-        n = s.layer_elems
-        out = prefill_bits_np(np.arange(layer * n, (layer + 1) * n, dtype=np.int64), self.prefill_seed(2 + which))
-        flat = out.reshape(s.pool_slots, s.num_kv_heads, s.head_dim)
-        for ri, r in enumerate(self.requests):
-            k, v = self.raw_layer(ri, layer)
-            vals = (k if which == 0 else v)[:r.suffix_tokens]
-            rows = r.src_row0 + np.arange(r.suffix_tokens)
-            slots = r.src_page_table[rows // s.page_size].astype(np.int64) * s.page_size + rows % s.page_size
-            flat[slots] = to_cache_bits(vals, s.out_dtype)
-        return out.reshape(s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim)
+        flat = np.full((s.pool_slots, s.num_kv_heads, s.head_dim), cache_nan_bits(s.out_dtype), dtype=np.uint16)
+        for ri in range(len(self.requests)):
+            slots, k, v = self.suffix_bits(ri, layer)
+            flat[slots] = k if which == 0 else v
+        return flat.reshape(s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim)
 
     def host_old_caches(self) -> Tuple[np.ndarray, np.ndarray]:
         """Old K and V caches ``[L, src_pool_pages, P, H, D]`` (small cases)."""
@@ -384,7 +251,7 @@ class Case:
         return (np.stack([self.old_cache_layer(0, l) for l in range(L)]),
                 np.stack([self.old_cache_layer(1, l) for l in range(L)]))
 
-    # -- raw draws and encoded layers ------------------------------------
+    # -- raw draws ---------------------------------------------------------
     def source_layer(self, layer: int) -> int:
         return layer % self.distinct_layers
 
@@ -393,29 +260,16 @@ class Case:
         return draw_layer(self.shape, self.seed, req_index, self.source_layer(layer), r.suffix_tokens,
                           self.outlier_pairs)
 
-    def encoded_layer(self, req_index: int, layer: int) -> Tuple[np.ndarray, np.ndarray]:
-        key = (req_index, self.source_layer(layer))
-        if key not in self._layer_cache:
-            k, v = self.raw_layer(req_index, layer)
-            self._layer_cache[key] = encode_layer(self.shape, self.requests[req_index], k, v)
-        return self._layer_cache[key]
-
-    def warm(self, workers: Optional[int] = None) -> None:
-        """Encode every distinct (request, layer) once, in parallel processes."""
-        keys = [(ri, l) for ri in range(len(self.requests)) for l in range(min(self.distinct_layers,
-                                                                                self.shape.num_layers))]
-        keys = [k for k in keys if k not in self._layer_cache]
-        if not keys:
-            return
-        workers = workers or default_workers()
-        if workers <= 1 or len(keys) == 1:
-            for ri, l in keys:
-                self.encoded_layer(ri, l)
-            return
-        args = [(self.shape, self.requests[ri], self.seed, ri, l, self.outlier_pairs) for ri, l in keys]
-        with ProcessPoolExecutor(max_workers=min(workers, len(keys))) as ex:
-            for key, res in zip(keys, ex.map(_encode_job, args)):
-                self._layer_cache[key] = res
+    def suffix_bits(self, req_index: int, layer: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+        """(old slots [N], K bits [N, H, D], V bits [N, H, D]) of one request's
+        suffix rows in one layer of the old caches (cache dtype)."""
+        r = self.requests[req_index]
+        k, v = self.raw_layer(req_index, layer)
+        P = self.shape.page_size
+        rows = r.src_row0 + np.arange(r.suffix_tokens)
+        slots = r.src_page_table[rows // P].astype(np.int64) * P + rows % P
+        return (slots, to_cache_bits(k[:r.suffix_tokens], self.shape.out_dtype),
+                to_cache_bits(v[:r.suffix_tokens], self.shape.out_dtype))
 
     def layer_payload_offset(self, req_index: int, layer: int) -> int:
         r = self.requests[req_index]
@@ -424,19 +278,6 @@ class Case:
     def layer_scale_offset(self, req_index: int, layer: int) -> int:
         r = self.requests[req_index]
         return r.scale_offset + layer * r.num_blocks * self.shape.num_kv_heads * 4
-
-    def host_payload(self) -> Tuple[np.ndarray, np.ndarray]:
-        """Full (payload uint8, scales uint16) host arrays."""
-        payload = np.zeros(self.payload_nbytes, dtype=np.uint8)
-        scales = np.full(self.scale_elems, FP16_NAN_BITS, dtype=np.uint16)
-        for ri, r in enumerate(self.requests):
-            for l in range(self.shape.num_layers):
-                pb, sb = self.encoded_layer(ri, l)
-                o = self.layer_payload_offset(ri, l)
-                payload[o:o + pb.size] = pb
-                so = self.layer_scale_offset(ri, l)
-                scales[so:so + sb.size] = sb.reshape(-1)
-        return payload, scales
 
     # -- pool ------------------------------------------------------------
     def prefill_seed(self, which: int) -> int:
@@ -481,21 +322,19 @@ class Case:
                 "total": L * (read + scales + written)}
 
 
+def cache_nan_bits(out_dtype: int) -> int:
+    return FP16_NAN_BITS if out_dtype == OUT_FP16 else 0x7FC0
+
+
 def to_cache_bits(x: np.ndarray, out_dtype: int) -> np.ndarray:
-    """Bit patterns of float values stored in a fp16 or bf16 cache (the
-    libraries' own round-to-nearest-even conversions)."""
-    x = np.asarray(x, dtype=np.float32)
+    """Bit patterns of finite float values stored in a fp16 or bf16 cache
+    (round to nearest even; no torch, so it is safe in forked workers)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
     if out_dtype == OUT_FP16:
         return x.astype(np.float16).view(np.uint16)
-    import torch
-
-    return torch.from_numpy(np.ascontiguousarray(x)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
-
-
-def _encode_job(args):
-    shape, req, seed, ri, l, outlier_pairs = args
-    k, v = draw_layer(shape, seed, ri, l, req.suffix_tokens, outlier_pairs)
-    return encode_layer(shape, req, k, v)
+    assert np.isfinite(x).all()
+    b = x.view(np.uint32)
+    return ((b + (((b >> 16) & 1) + 0x7FFF)) >> 16).astype(np.uint16)
 
 
 def default_workers() -> int:

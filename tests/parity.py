@@ -74,11 +74,107 @@ def log(msg: str) -> None:
     sys.stdout.flush()
 
 
-def check_full(dr) -> Stats:
-    """Whole-cache comparison against a full oracle restore (small cases)."""
+# ---------------------------------------------------------------------------
+# Checkpoints for the restore tests
+# ---------------------------------------------------------------------------
+
+POISON_BYTE = 0xFF        # an FP16 tile of 0xFFFF is NaN
+POISON_SCALE = 0x7E00     # binary16 NaN: a quantised tile decodes to NaN
+
+
+def oracle_checkpoint(case, poison: bool = True):
+    """(payload uint8, scales uint16) of a small case, written by the oracle's
+    quantize-and-gather from the case's old caches; with ``poison`` every
+    repair block's tiles and scales are overwritten with NaN encodings, so a
+    restore that reads one shows it."""
+    from oracle import quantize as oq
+
+    k_old, v_old = case.host_old_caches()
+    payload, scales = oq.quantize_gather(case.src_shape, case.requests, k_old, v_old,
+                                         case.payload_nbytes, case.scale_elems)
+    if poison:
+        pr, sr = repair_ranges(case)
+        for a, b in pr:
+            payload[a:b] = POISON_BYTE
+        for a, b in sr:
+            scales[a:b] = POISON_SCALE
+    return payload, scales
+
+
+def repair_ranges(case):
+    """Half-open (payload byte ranges, scale element ranges) of every repair
+    block's K and V tiles and scales, all layers, adjacent ranges merged."""
+    s = case.shape
+    B, H, D = s.block_tokens, s.num_kv_heads, s.head_dim
+    pr, sr = [], []
+    for ri, req in enumerate(case.requests):
+        layout = oracle.block_layout(req.tags, B, H, D)[0]
+        for layer in range(s.num_layers):
+            po = case.layer_payload_offset(ri, layer)
+            so = case.layer_scale_offset(ri, layer)
+            for b in range(len(req.tags)):
+                if not req.repair[b]:
+                    continue
+                tag = int(req.tags[b])
+                k0, v0 = layout[b]
+                pr.append((po + k0, po + v0 + B * H * D * oracle.VALUE_BITS[tag] // 8))
+                sr.append((so + b * H * 4, so + (b + 1) * H * 4))
+    return _merge(pr), _merge(sr)
+
+
+def _merge(ranges):
+    out = []
+    for a, b in sorted(ranges):
+        if out and a <= out[-1][1]:
+            out[-1] = (out[-1][0], max(out[-1][1], b))
+        else:
+            out.append((a, b))
+    return out
+
+
+def poison_device(case, payload, scales) -> None:
+    """:func:`oracle_checkpoint`'s poisoning applied to device buffers."""
+    pr, sr = repair_ranges(case)
+    for a, b in pr:
+        payload[a:b].fill_(POISON_BYTE)
+    nan = POISON_SCALE - 65536 if POISON_SCALE >= 32768 else POISON_SCALE
+    for a, b in sr:
+        scales[a:b].fill_(nan)
+
+
+def oracle_layer_checkpoint(case, ri: int, layer: int):
+    """The oracle's checkpoint of one (request, layer) from the drawn rows:
+    (payload bytes, scale bits [NB, H, 2, 2])."""
+    from oracle import quantize as oq
+
+    _, kb, vb = case.suffix_bits(ri, layer)
+    return oq.quantize_rows(case.shape, case.requests[ri], kb, vb)
+
+
+def restore_small(case, poison: bool = True):
+    """Restore a small case on the GPU from the oracle's checkpoint.
+    Returns (DeviceRestore after one run, (payload, scales) on the host)."""
+    import torch
+
+    from paper_2609_26219_amd.device import DeviceRestore
+
+    ckpt = oracle_checkpoint(case, poison)
+    dr = DeviceRestore(case, checkpoint=ckpt)
+    dr.run()
+    torch.cuda.synchronize()
+    return dr, ckpt
+
+
+# ---------------------------------------------------------------------------
+# Comparisons
+# ---------------------------------------------------------------------------
+
+def check_full(dr, ckpt) -> Stats:
+    """Whole-cache comparison against a full oracle restore from the same
+    checkpoint (small cases)."""
     case = dr.case
     s = case.shape
-    payload, scales = case.host_payload()
+    payload, scales = ckpt
     pre_k, pre_v = case.host_prefill(0), case.host_prefill(1)
     k_got, v_got = dr.host_caches()
     written = oracle.written_slots(s, case.requests)
@@ -99,18 +195,32 @@ def check_full(dr) -> Stats:
     return st
 
 
-def check_sampled(dr, samples, check_untouched: bool = True) -> Stats:
-    """Compare every reused block of the sampled (request, layer) pairs; check
-    all untouched elements of every layer on the device."""
+def check_device_checkpoint(case, payload, scales, refs) -> None:
+    """Bit-exact comparison of device-written checkpoint slices with the
+    oracle's, for the (request, layer) keys of ``refs``."""
+    for (ri, layer), (pb, sb) in refs.items():
+        po = case.layer_payload_offset(ri, layer)
+        so = case.layer_scale_offset(ri, layer)
+        got_p = payload[po:po + pb.size].cpu().numpy()
+        got_s = scales[so:so + sb.size].cpu().numpy().view(np.uint16)
+        bad_p = int((got_p != pb).sum())
+        bad_s = int((got_s != sb.reshape(-1)).sum())
+        log(f"  checkpoint request {ri} layer {layer}: {pb.size} bytes, {sb.size} scales, "
+            f"{bad_p} + {bad_s} mismatches")
+        assert bad_p == 0 and bad_s == 0
+
+
+def check_sampled(dr, refs, check_untouched: bool = True) -> Stats:
+    """Compare every reused block of the sampled (request, layer) pairs with
+    the oracle's restore of the oracle's checkpoint ``refs[(request, layer)]``;
+    check all untouched elements of every layer on the device."""
     case = dr.case
     s = case.shape
     st = Stats()
-    for ri, layer in samples:
+    shape1 = dataclasses.replace(s, num_layers=1)
+    for (ri, layer), (pb, sb) in refs.items():
         req = case.requests[ri]
-        pb, sb = case.encoded_layer(ri, layer)
-        # a one-layer view of this request's checkpoint for the oracle
-        one = dataclasses.replace(req, payload_offset=0, scale_offset=0) if dataclasses.is_dataclass(req) else req
-        shape1 = dataclasses.replace(s, num_layers=1)
+        one = dataclasses.replace(req, payload_offset=0, scale_offset=0)
         blocks = oracle.reused_blocks(req)
         all_slots = np.concatenate([oracle.destination_slots(s, req, b) for b in blocks]) if blocks else np.zeros(0, int)
         kg = dr.rows(0, layer, all_slots)

@@ -13,7 +13,9 @@ import numpy as np
 import pytest
 
 import oracle
+from oracle import quantize as oq
 from paper_2609_26219_amd import workloads as wl
+from parity import oracle_checkpoint
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -72,8 +74,10 @@ def test_decode_within_half_step(tag):
     case = wl.make_custom(7 + tag, H=3, D=32, B=8, n_tokens=(77,), deltas=(3,), rho0s=(5,), tag_set=(tag,),
                           mix=(1.0,), repair_frac=0.0, outlier_pairs=1)
     req = case.requests[0]
-    payload, scales = case.host_payload()
-    k_raw, v_raw = case.raw_layer(0, 0)
+    payload, scales = oracle_checkpoint(case)
+    _, kb, vb = case.suffix_bits(0, 0)
+    k_raw = oq.cache_values(kb, case.shape.out_dtype)
+    v_raw = oq.cache_values(vb, case.shape.out_dtype)
     B, H, D = case.shape.block_tokens, case.shape.num_kv_heads, case.shape.head_dim
     for b in range(req.num_blocks):
         n = oracle.valid_tokens(req, B, b)
@@ -96,10 +100,10 @@ def test_constant_tile_decodes_exactly():
                 rope_theta=1e4, out_dtype=0)
     req = _NS(suffix_tokens=2, delta=0, dst_row0=0, tags=np.array([wl.TAG_K8V8], np.uint8),
               repair=np.zeros(1, np.uint8), page_table=np.array([1], np.int32), payload_offset=0, scale_offset=0)
-    x = np.full((1, 2, 1, 4), 1.25, dtype=np.float32)
+    x = np.full((2, 4), 1.25)
     for bits in (8, 4):
-        codes, s, z = wl.quantize_tiles(x, np.array([2]), bits)
-        assert float(s[0, 0]) == 0.0 and float(z[0, 0]) == 1.25 and (codes == 0).all()
+        codes, s, z = oq.quantize_tile(x, bits)
+        assert s == 0 and z == 0x3D00 and (codes == 0).all()
     payload = np.zeros(16, np.uint8)
     scales = np.array([0, 0x3D00, 0, 0x3D00], np.uint16)  # scale 0, zero 1.25 for K and V
     k, v = oracle.decode_block(payload, scales, shape, req, 0, 0)
@@ -110,7 +114,7 @@ def test_nibble_order_low_is_even_channel():
     raw = np.array([0x21, 0xC3], np.uint8)
     codes = oracle.read_tile(raw, 0, 4, 1, 1, 4)
     assert codes.reshape(-1).tolist() == [1, 2, 3, 12]
-    assert wl.pack_nibbles(np.array([1, 2, 3, 12], np.uint8)).tolist() == [0x21, 0xC3]
+    assert oq.pack_tile(np.array([[[1, 2, 3, 12]]], np.uint8), 4).tolist() == [0x21, 0xC3]
 
 
 # ---------------------------------------------------------------------------
@@ -193,7 +197,7 @@ def test_zero_shift_is_identity_even_for_signed_zero():
 
 def test_values_never_rotated():
     case = wl.make_custom(5, n_tokens=(70, 33), deltas=(9, -4), out_dtype=wl.OUT_BF16)
-    payload, scales = case.host_payload()
+    payload, scales = oracle_checkpoint(case)
     pre_k, pre_v = case.host_prefill(0), case.host_prefill(1)
     _, v1 = oracle.restore(case.shape, case.requests, payload, scales, pre_k, pre_v)
     for r in case.requests:
@@ -205,7 +209,7 @@ def test_values_never_rotated():
 def test_fp16_tag_zero_shift_fp16_output_is_bit_identity():
     case = wl.make_custom(2, H=2, D=64, B=16, n_tokens=(90,), deltas=(0,), rho0s=(7,), tag_set=(wl.TAG_FP16,),
                           mix=(1.0,), repair_frac=0.0)
-    payload, scales = case.host_payload()
+    payload, scales = oracle_checkpoint(case)
     req = case.requests[0]
     k, v = oracle.restore(case.shape, case.requests, payload, scales, case.host_prefill(0), case.host_prefill(1))
     kf = k.reshape(-1, case.shape.row_elems)
@@ -230,7 +234,7 @@ def test_placement_brute_force(seed):
     case = wl.make_custom(seed, L=2, H=2, D=32, B=8, P=4, n_tokens=(37, 16, 5), deltas=(3, 0, -7),
                           rho0s=(0, 6, 13), repair_frac=0.3)
     s = case.shape
-    payload, scales = case.host_payload()
+    payload, scales = oracle_checkpoint(case)
     pre_k, pre_v = case.host_prefill(0), case.host_prefill(1)
     k, v = oracle.restore(s, case.requests, payload, scales, pre_k, pre_v)
     # Dense logical rows per request: row -> rounded K/V of that row.
@@ -273,7 +277,7 @@ def test_placement_brute_force(seed):
 
 def test_untouched_slots_and_repair_blocks_unread():
     case = wl.make_case("tiny")
-    payload, scales = case.host_payload()
+    payload, scales = oracle_checkpoint(case)
     pre_k, pre_v = case.host_prefill(0), case.host_prefill(1)
     k, v = oracle.restore(case.shape, case.requests, payload, scales, pre_k, pre_v)
     mask = oracle.written_slots(case.shape, case.requests)
@@ -281,7 +285,7 @@ def test_untouched_slots_and_repair_blocks_unread():
     kf, vf = k.reshape(s.num_layers, -1, s.row_elems), v.reshape(s.num_layers, -1, s.row_elems)
     pk, pv = pre_k.reshape(kf.shape), pre_v.reshape(vf.shape)
     assert np.array_equal(kf[:, ~mask], pk[:, ~mask]) and np.array_equal(vf[:, ~mask], pv[:, ~mask])
-    # repair blocks hold NaN poison: nothing written may be NaN
+    # repair blocks hold NaN encodings: nothing written may be NaN
     for arr in (kf[:, mask], vf[:, mask]):
         assert not np.isnan(arr.view(np.float16).astype(np.float32)).any()
     assert int(mask.sum()) == case.restored_tokens()
@@ -289,7 +293,7 @@ def test_untouched_slots_and_repair_blocks_unread():
 
 def test_placement_rejects_bad_pages():
     case = wl.make_custom(4, n_tokens=(40,), deltas=(1,), rho0s=(3,), repair_frac=0.0)
-    payload, scales = case.host_payload()
+    payload, scales = oracle_checkpoint(case)
     req = case.requests[0]
     req.page_table = req.page_table.copy()
     req.page_table[1] = -1
@@ -311,8 +315,9 @@ def test_payload_size_closed_form():
         per_token_head = {0: 4 * s.head_dim, 1: 2 * s.head_dim, 2: 1.5 * s.head_dim, 3: s.head_dim}
         closed = s.num_layers * s.block_tokens * s.num_kv_heads * sum(per_token_head[int(t)] for t in req.tags)
         assert oracle.request_payload_bytes(s, req) == closed == wl.encoded_request_nbytes(s, req)[0]
-        pb, sb = case.encoded_layer(0, 0)
-        assert pb.size * s.num_layers == closed
+        k_old, v_old = case.old_cache_layer(0, 0), case.old_cache_layer(1, 0)
+        pb, sb = oq.quantize_layer(case.src_shape, req, k_old, v_old)
+        assert pb.size * s.num_layers == closed and sb.size == len(req.tags) * s.num_kv_heads * 4
 
 
 def test_payload_ratios_match_paper_microbenchmark():

@@ -125,3 +125,17 @@ def test_write_then_read_cycle_recovers_values():
                     sz = oracle.block_scales(scales, dst, shape, layer, b)
                     step = sz[:, 0 if cache is k else 1, 0][None, :, None]
                     assert (np.abs(got - want) <= step / 2 * (1 + 1e-12)).all()
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_layer_form_equals_tile_by_tile(seed):
+    """The vectorised per-layer form gives the same bytes as the per-tile form."""
+    from paper_2609_26219_amd import workloads as wl
+    for dtype in (wl.OUT_FP16, wl.OUT_BF16):
+        case = wl.make_custom(seed, L=2, H=3, D=32, B=8, P=4, n_tokens=(37, 5, 16), deltas=(3, 0, -2),
+                              rho0s=(9, 4, 30), tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), out_dtype=dtype,
+                              outlier_pairs=1)
+        k, v = case.host_old_caches()
+        a = oq.quantize_gather(case.src_shape, case.requests, k, v, case.payload_nbytes, case.scale_elems)
+        b = oq.quantize_gather_per_tile(case.src_shape, case.requests, k, v, case.payload_nbytes, case.scale_elems)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])

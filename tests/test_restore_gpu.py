@@ -9,7 +9,8 @@ import oracle
 from paper_2609_26219_amd import binding as pb
 from paper_2609_26219_amd import workloads as wl
 
-from parity import check_full, check_sampled, log
+from parity import (check_device_checkpoint, check_full, check_sampled, log, oracle_checkpoint,
+                    oracle_layer_checkpoint, poison_device, restore_small)
 
 pytestmark = pytest.mark.gpu
 
@@ -23,26 +24,17 @@ def torch():
     return _t
 
 
-def _run(case, torch):
-    from paper_2609_26219_amd.device import DeviceRestore
-    dr = DeviceRestore(case)
-    dr.run()
-    torch.cuda.synchronize()
-    return dr
-
-
 @pytest.mark.parametrize("name", ["tiny", "llama8b_1l"])
 def test_named_small_full(name, torch):
     log(f"[gpu] {name}: full-cache parity")
-    dr = _run(wl.make_case(name), torch)
-    st = check_full(dr)
+    dr, ckpt = restore_small(wl.make_case(name))
+    st = check_full(dr, ckpt)
     log(f"  {st}")
     assert st.bit_exact_fraction > 0.9999
 
 
 def test_tiny_k4v4_reading(torch):
-    dr = _run(wl.make_case("tiny", int4_tag=wl.TAG_K4V4), torch)
-    check_full(dr)
+    check_full(*restore_small(wl.make_case("tiny", int4_tag=wl.TAG_K4V4)))
 
 
 PROPERTY_CASES = [
@@ -64,12 +56,12 @@ def test_property_cases(params, torch):
     case = wl.make_custom(hash(params) & 0xFFFF, L=2, H=H, D=D, B=B, P=P, n_tokens=n, deltas=deltas, rho0s=rho0s,
                           tag_set=tags, mix=[1.0] * len(tags), repair_frac=rep, out_dtype=out, outlier_pairs=1)
     log(f"[gpu] property case {params}")
-    check_full(_run(case, torch))
+    check_full(*restore_small(case))
 
 
 def test_all_repair_writes_nothing(torch):
     case = wl.make_custom(21, L=2, n_tokens=(64, 20), deltas=(4, 2), repair_all=True)
-    dr = _run(case, torch)
+    dr, _ = restore_small(case)
     assert dr.info["num_units"] == 0
     k, v = dr.host_caches()
     assert np.array_equal(k, case.host_prefill(0)) and np.array_equal(v, case.host_prefill(1))
@@ -78,14 +70,15 @@ def test_all_repair_writes_nothing(torch):
 def test_fp16_tag_zero_shift_is_bit_copy(torch):
     case = wl.make_custom(22, H=8, D=128, B=32, P=16, n_tokens=(300,), deltas=(0,), rho0s=(13,),
                           tag_set=(wl.TAG_FP16,), mix=(1.0,), repair_frac=0.1, out_dtype=wl.OUT_FP16)
-    st = check_full(_run(case, torch))
+    st = check_full(*restore_small(case))
     assert st.n_bit_exact == st.n
 
 
 def test_restore_is_repeatable_and_plan_reusable(torch):
     from paper_2609_26219_amd.device import DeviceRestore
     case = wl.make_case("tiny")
-    dr = DeviceRestore(case)
+    ckpt = oracle_checkpoint(case)
+    dr = DeviceRestore(case, checkpoint=ckpt)
     dr.run()
     dr.run()
     torch.cuda.synchronize()
@@ -101,12 +94,14 @@ def test_restore_is_repeatable_and_plan_reusable(torch):
     b = k1.reshape(a.shape)
     assert np.array_equal(a[:, written], b[:, written])
     assert (a[:, ~written] == 0).all()
-    check_full(dr)
+    check_full(dr, ckpt)
 
 
 def test_restore_argument_errors(torch):
     from paper_2609_26219_amd.device import DeviceRestore
-    dr = DeviceRestore(wl.make_case("tiny"))
+    case = wl.make_case("tiny")
+    ckpt = oracle_checkpoint(case)
+    dr = DeviceRestore(case, checkpoint=ckpt)
     nb = lambda t: t.numel() * t.element_size()
     p, s, k, v = dr.payload, dr.scales, dr.k_cache, dr.v_cache
     good = (p.data_ptr(), nb(p), s.data_ptr(), nb(s), k.data_ptr(), v.data_ptr(), nb(k), 0)
@@ -124,40 +119,51 @@ def test_restore_argument_errors(torch):
     ]
     for args in bad:
         assert pb.pkv_restore_status(dr.plan, *args) == pb.PKV_ERR_INVALID_ARGUMENT, args
-    check_full(dr)  # nothing above wrote anything
+    check_full(dr, ckpt)  # nothing above wrote anything
 
 
 def test_streams(torch):
     from paper_2609_26219_amd.device import DeviceRestore
-    dr = DeviceRestore(wl.make_case("llama8b_1l"))
+    case = wl.make_case("llama8b_1l")
+    ckpt = oracle_checkpoint(case)
+    dr = DeviceRestore(case, checkpoint=ckpt)
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
         dr.run()
     s.synchronize()
-    check_full(dr)
+    check_full(dr, ckpt)
 
 
 # ---------------------------------------------------------------------------
-# Full-size workloads, sampled outputs
+# Full-size workloads: the checkpoint is written on the GPU by
+# pkv_quantize_gather from the drawn old caches (layer by layer), compared
+# bit for bit with the oracle's on the sampled (request, layer) pairs, then
+# repair blocks are poisoned and the restore is compared with the oracle's
+# restore of the oracle's checkpoint on those pairs.
 # ---------------------------------------------------------------------------
+
+def _full_size(case, samples, torch):
+    from paper_2609_26219_amd.device import DeviceRestore
+    dr = DeviceRestore(case)
+    refs = {key: oracle_layer_checkpoint(case, *key) for key in samples}
+    check_device_checkpoint(case, dr.payload, dr.scales, refs)
+    poison_device(case, dr.payload, dr.scales)
+    dr.run()
+    torch.cuda.synchronize()
+    return check_sampled(dr, refs)
+
 
 def test_llama8b_32l_full_size(torch):
-    log("[gpu] llama8b_32l: full-size restore, 3 sampled layers + untouched check")
-    case = wl.make_case("llama8b_32l")
-    dr = _run(case, torch)
-    st = check_sampled(dr, [(0, 0), (0, 17), (0, 31)])
+    log("[gpu] llama8b_32l: full-size checkpoint + restore, 3 sampled layers + untouched check")
+    st = _full_size(wl.make_case("llama8b_32l"), [(0, 0), (0, 17), (0, 31)], torch)
     log(f"  {st}")
 
 
 def test_llama70b_full_size(torch):
-    log("[gpu] llama70b: full-size restore, 2 sampled layers + untouched check")
-    case = wl.make_case("llama70b", distinct_layers=2)
-    dr = _run(case, torch)
-    check_sampled(dr, [(0, 1), (0, 78)])
+    log("[gpu] llama70b: full-size checkpoint + restore, 2 sampled layers + untouched check")
+    _full_size(wl.make_case("llama70b", distinct_layers=2), [(0, 1), (0, 78)], torch)
 
 
 def test_batched16_full_size(torch):
     log("[gpu] batched16: 16 requests on a 2^20-slot pool, 4 sampled (request, layer) + untouched check")
-    case = wl.make_case("batched16", distinct_layers=1)
-    dr = _run(case, torch)
-    check_sampled(dr, [(0, 0), (5, 13), (11, 31), (15, 7)])
+    _full_size(wl.make_case("batched16", distinct_layers=1), [(0, 0), (5, 13), (11, 31), (15, 7)], torch)

@@ -292,7 +292,7 @@ def main():
                 "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s",
                 "frac": round(w_achieved / HBM_PEAK_GBPS, 4),
-                "traffic": measured_traffic(args.workload, args.int4, "gather_kernel", GATHER_SRC),
+                "traffic": measured_traffic(args.workload, args.int4, "gather_tile_kernel", GATHER_SRC),
             },
         },
     }

@@ -3,21 +3,34 @@
 // binary16 scale and zero, pack FP16 / 8-bit / 4-bit codes and place them in
 // the clustered checkpoint layout that the restore kernel reads.
 //
-// One workgroup encodes one (request, layer, block): every head, every row
-// (padding rows of a partial last block are written as code 0 / +0).  A
-// thread owns the same piece as in the restore kernel -- channels [8j, 8j+8)
-// and [D/2+8j, D/2+8j+8) of one head -- for up to 4 tokens, and keeps the
-// block's values in registers between the min/max pass and the encode pass,
-// so the cache is read once.  The per-head min and max are combined with LDS
-// integer atomics on order-preserving keys of the float values.
+// Work is split into tiles, one per (request, layer, block, K|V, head); one
+// wave encodes one tile.  A wave's lanes cover a head's row in pieces of 8
+// channels (D/8 lanes per row, 64/(D/8) rows per load), so the tile's
+// min/max is a wave reduction: no LDS and no barrier.  A lane holds its rows
+// in NL 16-byte registers between the range pass and the encode pass.
+//
+// Two kernels.  The tile kernel (blocks whose tile fits NL <= 8 loads per lane
+// and spans at most three cache pages, layer slices below 4 GiB) takes the
+// block's source pages from its work item, so no page-table load sits in
+// front of the row loads; it uses 32-bit buffer offsets, consumes every
+// loaded register on every path, and issues every store (lanes with nothing
+// to write get an offset the hardware drops), which keeps register use low
+// and occupancy high.  The general kernel (any valid model) reads the page
+// table per row and reads a tile twice when it needs more than 16 loads per
+// lane (range pass, then encode pass).  In
+// both, the waves of one workgroup encode the heads of one (block, K|V), so
+// they write neighbouring pieces of the same rows into one L2.
 //
 // Arithmetic follows the format's definition exactly: the zero is the
 // largest binary16 not above the minimum, the scale the smallest binary16
-// not below (max - zero)/(2^bits - 1) (both computed in double), and a code
-// is round-half-even((x - zero)/scale).  The quotient is formed as
-// (x - zero) * (1/scale) in double and, whenever that lands within 1e-6 of a
-// rounding boundary, recomputed with a true division, so the codes equal those
-// of a correctly rounded division.
+// not below (max - zero)/(2^bits - 1) (both in double), and a code is
+// round-half-even((x - zero)/scale) with the quotient correctly rounded in
+// double.  Codes are first formed in float as floor((x - zero) * (1/scale) +
+// 1/2); that float value is within 5e-5 of the exact quotient + 1/2 (three
+// roundings of 2^-24 relative on a quotient <= 255, plus the final one), so
+// whenever it lies farther than 1e-4 from an integer its floor is the exact
+// rounding; a packed word of codes (8 four-bit or 4 eight-bit) with any value
+// closer is recomputed in double with a true division.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -29,6 +42,10 @@
 namespace pkv {
 namespace {
 
+#ifndef GATHER_MIN_WAVES
+#define GATHER_MIN_WAVES 1
+#endif
+
 struct GatherArgs {
   const Unit* units;
   const int32_t* page_tables;
@@ -37,22 +54,23 @@ struct GatherArgs {
   uint8_t* payload;
   uint16_t* scales;
   int64_t layer_elems;
-  int32_t H, D, B, log2P, cols, tpp;
+  int32_t H, D, B, log2P;
+  int32_t lpr;     // lanes per row: D / 8
+  int32_t rpl;     // rows per load: 64 / lpr
+  int32_t nchunk;  // register-resident chunks of NL loads per lane covering the block
 };
 
-__device__ __forceinline__ int32_t order_key(float f) {
-  const int32_t b = __float_as_int(f);
-  return b ^ ((b >> 31) & 0x7FFFFFFF);
-}
-__device__ __forceinline__ float from_order_key(int32_t k) { return __int_as_float(k ^ ((k >> 31) & 0x7FFFFFFF)); }
-
 template <bool BF16>
-__device__ __forceinline__ float cache_value(uint32_t bits16) {
+__device__ __forceinline__ float cache_value(uint32_t word, int half) {
   if constexpr (BF16) {
-    return __uint_as_float(bits16 << 16);
+    return __uint_as_float(half ? (word & 0xFFFF0000u) : (word << 16));
   } else {
-    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(half ? word >> 16 : word)));
   }
+}
+
+__device__ __forceinline__ uint32_t word_of(const uint4& w, int e) {
+  return e < 2 ? w.x : e < 4 ? w.y : e < 6 ? w.z : w.w;
 }
 
 // binary16 helpers.  The double -> binary16 cast is a single correctly
@@ -80,20 +98,59 @@ __device__ __forceinline__ uint16_t f16_ceil(double x) {
   return f16_value(h) < x ? f16_next_up(h) : h;
 }
 
-__device__ __forceinline__ uint32_t element(const uint4& w, int e) {
-  const uint32_t word = e < 2 ? w.x : e < 4 ? w.y : e < 6 ? w.z : w.w;
-  return (word >> (16 * (e & 1))) & 0xFFFFu;
+struct Quant {
+  float zf, invf;
+  uint32_t qmax;
+  double zero, scale;
+};
+
+// Codes of the first N values of w (x >= zero, scale > 0) packed into one
+// word: N = 8 four-bit codes (nibble e) or N = 4 eight-bit codes (byte e).
+// v = (x - zero) * (1/scale) + 1/2 is formed in float (fma, one rounding) and
+// the code is floor(v), clipped.  `near` is set when some v lies within 1e-4
+// of an integer, where the float quotient cannot decide the rounding; the
+// caller then uses encode_exact.
+template <bool BF16, int N>
+__device__ __forceinline__ uint32_t encode_fast(const uint4& w, const Quant& q, bool& near) {
+  constexpr int kBits = 32 / N;
+  uint32_t packed = 0;
+  bool tie = false;
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    const float x = cache_value<BF16>(word_of(w, e), e & 1);
+    const float v = __builtin_fmaf(x - q.zf, q.invf, 0.5f);
+    uint32_t k = static_cast<uint32_t>(v);  // v > 0: truncation is floor
+    k = k < q.qmax ? k : q.qmax;
+    const float f = __builtin_amdgcn_fractf(v);
+    tie |= __builtin_fabsf(f - 0.5f) > 0.4999f;
+    packed |= k << (kBits * e);
+  }
+  near = tie;
+  return packed;
 }
 
-// Code of one value: round-half-even((x - zero) / scale), clipped.
-__device__ __forceinline__ uint32_t encode(float x, double zero, double scale, double inv, double qmax) {
-  if (scale == 0.0) return 0;
-  const double d = static_cast<double>(x) - zero;  // exact
-  const double y = d * inv;
-  double k = __builtin_rint(y);
-  if (__builtin_fabs(__builtin_fabs(y - k) - 0.5) < 1e-6) k = __builtin_rint(d / scale);
-  k = k < 0.0 ? 0.0 : (k > qmax ? qmax : k);
-  return static_cast<uint32_t>(k);
+// The same codes from the definition in double: rint((x - zero) / scale)
+// with a correctly rounded division, clipped.
+template <bool BF16, int N>
+__device__ __forceinline__ uint32_t encode_exact(uint4 w, const Quant& q) {
+  constexpr int kBits = 32 / N;
+  uint32_t packed = 0;
+  for (int e = 0; e < N; ++e) {
+    const uint32_t word = e < 2 ? w.x : e < 4 ? w.y : e < 6 ? w.z : w.w;
+    const float x = cache_value<BF16>(word, e & 1);
+    double k = __builtin_rint((static_cast<double>(x) - q.zero) / q.scale);
+    k = k < 0.0 ? 0.0 : k;
+    const uint32_t c = static_cast<uint32_t>(k);
+    packed |= (c < q.qmax ? c : q.qmax) << (kBits * e);
+  }
+  return packed;
+}
+
+template <bool BF16, int N>
+__device__ __forceinline__ uint32_t encode_word(const uint4& w, const Quant& q) {
+  bool near;
+  const uint32_t packed = encode_fast<BF16, N>(w, q, near);
+  return near ? encode_exact<BF16, N>(w, q) : packed;
 }
 
 template <bool BF16>
@@ -104,143 +161,379 @@ __device__ __forceinline__ uint4 to_half8(const uint4& w) {
     uint32_t o[4];
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      const uint16_t lo = __builtin_bit_cast(uint16_t, static_cast<_Float16>(cache_value<true>(element(w, 2 * p))));
-      const uint16_t hi = __builtin_bit_cast(uint16_t, static_cast<_Float16>(cache_value<true>(element(w, 2 * p + 1))));
+      const uint32_t word = word_of(w, 2 * p);
+      const uint16_t lo = __builtin_bit_cast(uint16_t, static_cast<_Float16>(cache_value<true>(word, 0)));
+      const uint16_t hi = __builtin_bit_cast(uint16_t, static_cast<_Float16>(cache_value<true>(word, 1)));
       o[p] = uint32_t(lo) | (uint32_t(hi) << 16);
     }
     return make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
-// Encode one K or V tile of the unit's block (all rows) and its scales.
-template <bool BF16>
-__device__ void encode_tile(const GatherArgs& a, const Unit& u, const uint16_t* __restrict__ cache,
-                            uint8_t* __restrict__ tile, int which, int bits, int32_t* s_min, int32_t* s_max,
-                            bool active, int t0, int head, int j) {
-  const int H = a.H, D = a.D;
-  const int64_t slot_mask = (int64_t(1) << a.log2P) - 1;
-  const int64_t row_elems = int64_t(H) * D;
-  const int64_t lbase = int64_t(u.layer) * a.layer_elems + int64_t(head) * D;
-  uint4 lo[kGatherTokens], hi[kGatherTokens];
+// Lane-private view of one (block, head, K|V) tile.
+struct TileLane {
+  const uint16_t* src;  // cache + layer + head + lane's channel piece
+  uint8_t* tile;        // the tile's first byte
+  int64_t row0, pt_off, row_elems, slot_mask;
+  int32_t r, c, n_valid, log2P;
+  bool on;              // lane holds a piece of a row
+};
+
+template <int NL>
+__device__ __forceinline__ void load_chunk(const GatherArgs& a, const TileLane& L, int ch, uint4 (&w)[NL]) {
 #pragma unroll
-  for (int i = 0; i < kGatherTokens; ++i) {
-    lo[i] = make_uint4(0, 0, 0, 0);
-    hi[i] = make_uint4(0, 0, 0, 0);
-    const int t = t0 + i * a.tpp;
-    if (active && t < u.n_valid) {
-      const int64_t row = u.row0 + t;
-      const int64_t page = a.page_tables[u.pt_off + (row >> a.log2P)];
-      const uint16_t* src = cache + lbase + ((page << a.log2P) | (row & slot_mask)) * row_elems;
-      lo[i] = *reinterpret_cast<const uint4*>(src + 8 * j);
-      hi[i] = *reinterpret_cast<const uint4*>(src + D / 2 + 8 * j);
+  for (int i = 0; i < NL; ++i) {
+    const int t = (ch * NL + i) * a.rpl + L.r;
+    w[i] = make_uint4(0, 0, 0, 0);
+    if (L.on && t < L.n_valid) {
+      const int64_t row = L.row0 + t;
+      const int64_t page = a.page_tables[L.pt_off + (row >> L.log2P)];
+      w[i] = *reinterpret_cast<const uint4*>(L.src + ((page << L.log2P) | (row & L.slot_mask)) * L.row_elems);
     }
   }
-  const bool scale_writer = active && t0 == 0 && j == 0;
+}
+
+template <bool BF16, int NL>
+__device__ void encode_tile(const GatherArgs& a, const Unit& u, int which, int head, int r, int c, bool on) {
+  const int tag = u.tag & 0xFF;
+  const int bits = which ? kValueBits[tag] : kKeyBits[tag];
+  const int H = a.H, D = a.D;
+  TileLane L;
+  L.src = (which ? a.v_cache : a.k_cache) + int64_t(u.layer) * a.layer_elems + int64_t(head) * D + 8 * c;
+  L.tile = a.payload + (which ? u.v_off : u.k_off);
+  L.row0 = u.row0;
+  L.pt_off = u.pt_off;
+  L.row_elems = int64_t(H) * D;
+  L.slot_mask = (int64_t(1) << a.log2P) - 1;
+  L.r = r;
+  L.c = c;
+  L.n_valid = u.n_valid;
+  L.log2P = a.log2P;
+  L.on = on;
+  uint32_t* scale_word = reinterpret_cast<uint32_t*>(a.scales + u.scale_off + 4 * head + 2 * which);
+  const bool lane0 = (threadIdx.x & 63) == 0;
+  uint4 w[NL];
+
   if (bits == 16) {
+    for (int ch = 0; ch < a.nchunk; ++ch) {
+      load_chunk<NL>(a, L, ch, w);
 #pragma unroll
-    for (int i = 0; i < kGatherTokens; ++i) {
-      const int t = t0 + i * a.tpp;
-      if (active && t < a.B) {
-        uint8_t* row = tile + (int64_t(t) * H + head) * D * 2;
-        *reinterpret_cast<uint4*>(row + 16 * j) = to_half8<BF16>(lo[i]);
-        *reinterpret_cast<uint4*>(row + D + 16 * j) = to_half8<BF16>(hi[i]);
+      for (int i = 0; i < NL; ++i) {
+        const int t = (ch * NL + i) * a.rpl + r;
+        if (on && t < a.B)
+          *reinterpret_cast<uint4*>(L.tile + (int64_t(t) * H + head) * D * 2 + 16 * c) = to_half8<BF16>(w[i]);
       }
     }
-    if (scale_writer) {
-      *reinterpret_cast<uint32_t*>(a.scales + u.scale_off + 4 * head + 2 * which) = 0u;
-    }
+    if (lane0) *scale_word = 0u;
     return;
   }
-  // Per-head range over the valid rows.
+
+  // Range pass over the valid rows (padding rows load as 0 and are skipped).
+  float mn = __builtin_inff(), mx = -__builtin_inff();
+  for (int ch = 0; ch < a.nchunk; ++ch) {
+    load_chunk<NL>(a, L, ch, w);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int t = (ch * NL + i) * a.rpl + r;
+      if (on && t < L.n_valid) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = cache_value<BF16>(word_of(w[i], e), e & 1);
+          mn = __builtin_fminf(mn, x);
+          mx = __builtin_fmaxf(mx, x);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    mn = __builtin_fminf(mn, __shfl_xor(mn, off));
+    mx = __builtin_fmaxf(mx, __shfl_xor(mx, off));
+  }
+  const double qmax = double((1 << bits) - 1);
+  const double vmin = static_cast<double>(mn) + 0.0;  // -0 counts as +0
+  const uint16_t zb = f16_floor(vmin);
+  Quant q;
+  q.zero = f16_value(zb);
+  const uint16_t sb = f16_ceil(((static_cast<double>(mx) - q.zero) + 0.0) / qmax);  // -0 span counts as +0
+  q.scale = f16_value(sb);
+  q.zf = static_cast<float>(q.zero);
+  q.invf = q.scale != 0.0 ? static_cast<float>(1.0 / q.scale) : 0.0f;
+  q.qmax = uint32_t((1 << bits) - 1);
+  const bool flat = q.scale == 0.0;  // every value equals the zero: code 0
+
+  // Encode pass.
+  for (int ch = 0; ch < a.nchunk; ++ch) {
+    if (a.nchunk > 1) load_chunk<NL>(a, L, ch, w);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int t = (ch * NL + i) * a.rpl + r;
+      if (!(on && t < a.B)) continue;
+      const bool valid = t < L.n_valid && !flat;
+      if (bits == 8) {
+        uint2 v = make_uint2(0, 0);
+        if (valid) {
+          v.x = encode_word<BF16, 4>(make_uint4(w[i].x, w[i].y, 0, 0), q);
+          v.y = encode_word<BF16, 4>(make_uint4(w[i].z, w[i].w, 0, 0), q);
+        }
+        *reinterpret_cast<uint2*>(L.tile + (int64_t(t) * H + head) * D + 8 * c) = v;
+      } else {
+        const uint32_t v = valid ? encode_word<BF16, 8>(w[i], q) : 0u;
+        *reinterpret_cast<uint32_t*>(L.tile + (int64_t(t) * H + head) * (D / 2) + 4 * c) = v;
+      }
+    }
+  }
+  if (lane0) *scale_word = uint32_t(sb) | (uint32_t(zb) << 16);
+}
+
+template <bool BF16, int NL>
+__global__ __launch_bounds__(kGatherMaxWaves * 64, GATHER_MIN_WAVES) void gather_kernel(GatherArgs a) {
+  const Unit u = a.units[blockIdx.x >> 1];
+  const int which = blockIdx.x & 1;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nwaves = blockDim.x >> 6;
+  const int r = lane / a.lpr;
+  const int c = lane - r * a.lpr;
+  const bool on = r < a.rpl;
+  for (int head = wave; head < a.H; head += nwaves) encode_tile<BF16, NL>(a, u, which, head, r, c, on);
+}
+
+// ---------------------------------------------------------------------------
+// Tile kernel for blocks that fit in registers (NL <= 8 loads per lane)
+// and span at most three pages.  Workgroup b's wave w encodes tile
+// b * waves + w of the (unit, K|V, head) order; the unit header, with the
+// block's source pages, is one uniform scalar load; the tile's range is a DPP
+// wave reduction (no LDS traffic, no barrier).
+// ---------------------------------------------------------------------------
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_from(float identity, float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(identity), __float_as_int(v), CTRL, ROW_MASK, 0xF,
+                                                    false));
+}
+
+// Min and max over the 64 lanes (every lane active), as uniform values.
+__device__ __forceinline__ void wave_range(float& mn, float& mx) {
+  const float pinf = __builtin_inff(), ninf = -__builtin_inff();
+  mn = __builtin_fminf(mn, dpp_from<0x111, 0xF>(pinf, mn));  // row_shr:1
+  mx = __builtin_fmaxf(mx, dpp_from<0x111, 0xF>(ninf, mx));
+  mn = __builtin_fminf(mn, dpp_from<0x112, 0xF>(pinf, mn));  // row_shr:2
+  mx = __builtin_fmaxf(mx, dpp_from<0x112, 0xF>(ninf, mx));
+  mn = __builtin_fminf(mn, dpp_from<0x114, 0xF>(pinf, mn));  // row_shr:4
+  mx = __builtin_fmaxf(mx, dpp_from<0x114, 0xF>(ninf, mx));
+  mn = __builtin_fminf(mn, dpp_from<0x118, 0xF>(pinf, mn));  // row_shr:8
+  mx = __builtin_fmaxf(mx, dpp_from<0x118, 0xF>(ninf, mx));
+  mn = __builtin_fminf(mn, dpp_from<0x142, 0xA>(pinf, mn));  // row_bcast:15 into rows 1, 3
+  mx = __builtin_fmaxf(mx, dpp_from<0x142, 0xA>(ninf, mx));
+  mn = __builtin_fminf(mn, dpp_from<0x143, 0xC>(pinf, mn));  // row_bcast:31 into rows 2, 3
+  mx = __builtin_fmaxf(mx, dpp_from<0x143, 0xC>(ninf, mx));
+  mn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mn), 63));
+  mx = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mx), 63));
+}
+
+struct TileArgs {
+  GatherArgs g;
+  int64_t num_tiles;  // units * 2 * H
+};
+
+// Uniform description of one (unit, K|V, head) tile.
+struct TileHdr {
+  const uint16_t* src;  // cache + layer + head
+  uint32_t range;       // bytes from src to the end of the layer's cache slice
+  uint8_t* tile;
+  uint32_t tile_bytes;  // B * H * D * bits / 8
+  uint32_t* scale_word;
+  int64_t row0;
+  int32_t n_valid, bits, head, first_page;
+  int32_t page0, page1, page2;  // kUnitPages source pages
+};
+
+__device__ __forceinline__ TileHdr tile_header(const GatherArgs& a, const Unit* __restrict__ units, int64_t T) {
+  const int64_t per_unit = 2 * int64_t(a.H);
+  const int64_t ui = T / per_unit;
+  const int32_t rest = int32_t(T - ui * per_unit);
+  const int32_t which = rest >= a.H ? 1 : 0;
+  const int32_t head = rest - which * a.H;
+  const Unit u = units[ui];
+  const int tag = u.tag & 0xFF;
+  TileHdr h;
+  h.src = (which ? a.v_cache : a.k_cache) + int64_t(u.layer) * a.layer_elems + int64_t(head) * a.D;
+  h.range = uint32_t((a.layer_elems - int64_t(head) * a.D) * 2);
+  h.tile = a.payload + (which ? u.v_off : u.k_off);
+  h.scale_word = reinterpret_cast<uint32_t*>(a.scales + u.scale_off + 4 * head + 2 * which);
+  h.row0 = u.row0;
+  h.n_valid = u.n_valid;
+  h.bits = which ? kValueBits[tag] : kKeyBits[tag];
+  h.tile_bytes = uint32_t(a.B) * uint32_t(a.H) * uint32_t(a.D) * uint32_t(h.bits) / 8u;
+  h.head = head;
+  h.first_page = int32_t(u.row0 >> a.log2P);
+  h.page0 = __builtin_amdgcn_readfirstlane(u.page0);
+  h.page1 = __builtin_amdgcn_readfirstlane(u.page1);
+  h.page2 = __builtin_amdgcn_readfirstlane(u.page2);
+  return h;
+}
+
+// Every lane loads every one of its NL rows; rows past n_valid (and idle
+// lanes) read the block's first row instead, so the loads carry no branch and
+// stay in flight together.  Offsets are 32-bit from the tile's base (the
+// launch checks that a layer's cache slice is below 4 GiB); the buffer range
+// check returns zeros past the slice rather than faulting.
+template <int NL>
+__device__ __forceinline__ void load_tile(const GatherArgs& a, const TileHdr& h, int r, int c, uint4 (&w)[NL]) {
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(h.src), 0, h.range, 0x00020000);
+  const uint32_t row_bytes = uint32_t(a.H) * uint32_t(a.D) * 2u;
+  const uint32_t slot_mask = (1u << a.log2P) - 1;
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int t = i * a.rpl + r;
+    const int64_t row = h.row0 + (t < h.n_valid ? t : 0);
+    const int k = int32_t(row >> a.log2P) - h.first_page;  // 0, 1 or 2
+    const uint32_t page = uint32_t(h.page0 + (k >= 1 ? h.page1 - h.page0 : 0) + (k >= 2 ? h.page2 - h.page1 : 0));
+    const uint32_t off = ((page << a.log2P) | (uint32_t(row) & slot_mask)) * row_bytes + 16u * uint32_t(c);
+    w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0));
+  }
+}
+
+using u32x2 = __attribute__((ext_vector_type(2))) unsigned;
+using u32x4 = __attribute__((ext_vector_type(4))) unsigned;
+constexpr uint32_t kDropOffset = 0x80000000u;  // past every tile's range: the store is discarded
+
+// The packed word again, opaque to the optimiser, so the range pass's float
+// conversions are not kept alive (twice the registers) for the encode pass.
+__device__ __forceinline__ uint4 fresh(uint4 w) {
+  asm volatile("" : "+v"(w.x), "+v"(w.y), "+v"(w.z), "+v"(w.w));
+  return w;
+}
+
+// A tile's work in two steps.  tile_range consumes every loaded register
+// (the range pass; FP16 tiles are converted in place), so once it returns no
+// load of this tile is outstanding and the next tile's loads can be issued
+// without the hardware wait counts having to cover them.  tile_store then
+// encodes and writes; every store is issued (a lane with nothing to write
+// gets an offset past the tile's buffer range, which the hardware drops).
+template <bool BF16, int NL>
+__device__ __forceinline__ Quant tile_range(const GatherArgs& a, const TileHdr& h, int r, bool on, uint4 (&w)[NL],
+                                            uint16_t& sb, uint16_t& zb) {
+  Quant q;
+  if (h.bits == 16) {
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int t = i * a.rpl + r;
+      w[i] = t < h.n_valid ? to_half8<BF16>(w[i]) : make_uint4(0, 0, 0, 0);
+    }
+    sb = zb = 0;
+    return q;
+  }
   float mn = __builtin_inff(), mx = -__builtin_inff();
 #pragma unroll
-  for (int i = 0; i < kGatherTokens; ++i) {
-    const int t = t0 + i * a.tpp;
-    if (active && t < u.n_valid) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x0 = cache_value<BF16>(element(lo[i], e));
-        const float x1 = cache_value<BF16>(element(hi[i], e));
-        mn = __builtin_fminf(mn, __builtin_fminf(x0, x1));
-        mx = __builtin_fmaxf(mx, __builtin_fmaxf(x0, x1));
-      }
-    }
-  }
-  if (active) {
-    atomicMin(&s_min[head], order_key(mn));
-    atomicMax(&s_max[head], order_key(mx));
-  }
-  __syncthreads();
-  const double qmax = double((1 << bits) - 1);
-  const double vmin = static_cast<double>(from_order_key(s_min[head])) + 0.0;  // -0 counts as +0
-  const double vmax = static_cast<double>(from_order_key(s_max[head]));
-  const uint16_t zb = f16_floor(vmin);
-  const double zero = f16_value(zb);
-  const uint16_t sb = f16_ceil(((vmax - zero) + 0.0) / qmax);  // -0 span counts as +0
-  const double scale = f16_value(sb);
-  const double inv = scale != 0.0 ? 1.0 / scale : 0.0;
-#pragma unroll
-  for (int i = 0; i < kGatherTokens; ++i) {
-    const int t = t0 + i * a.tpp;
-    if (!(active && t < a.B)) continue;
-    uint32_t c[16];
-    const bool valid = t < u.n_valid;
+  for (int i = 0; i < NL; ++i) {
+    const int t = i * a.rpl + r;
+    float pmn = __builtin_inff(), pmx = -__builtin_inff();
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      c[e] = valid ? encode(cache_value<BF16>(element(lo[i], e)), zero, scale, inv, qmax) : 0u;
-      c[8 + e] = valid ? encode(cache_value<BF16>(element(hi[i], e)), zero, scale, inv, qmax) : 0u;
+      const float x = cache_value<BF16>(word_of(w[i], e), e & 1);
+      pmn = __builtin_fminf(pmn, x);
+      pmx = __builtin_fmaxf(pmx, x);
     }
-    const int64_t r = int64_t(t) * H + head;
-    if (bits == 8) {
-      uint8_t* row = tile + r * D;
-      const uint2 w0 = make_uint2(c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24),
-                                  c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
-      const uint2 w1 = make_uint2(c[8] | (c[9] << 8) | (c[10] << 16) | (c[11] << 24),
-                                  c[12] | (c[13] << 8) | (c[14] << 16) | (c[15] << 24));
-      *reinterpret_cast<uint2*>(row + 8 * j) = w0;
-      *reinterpret_cast<uint2*>(row + D / 2 + 8 * j) = w1;
-    } else {
-      uint8_t* row = tile + r * (D / 2);
-      uint32_t w0 = 0, w1 = 0;
+    const bool ok = on && t < h.n_valid;
+    mn = ok ? __builtin_fminf(mn, pmn) : mn;
+    mx = ok ? __builtin_fmaxf(mx, pmx) : mx;
+  }
+  wave_range(mn, mx);
+  const double qmax = double((1 << h.bits) - 1);
+  zb = f16_floor(static_cast<double>(mn) + 0.0);  // -0 counts as +0
+  q.zero = f16_value(zb);
+  sb = f16_ceil(((static_cast<double>(mx) - q.zero) + 0.0) / qmax);  // -0 span counts as +0
+  q.scale = f16_value(sb);
+  q.zf = static_cast<float>(q.zero);
+  q.invf = q.scale != 0.0 ? static_cast<float>(1.0 / q.scale) : 0.0f;
+  q.qmax = uint32_t((1 << h.bits) - 1);
+  return q;
+}
+
+template <bool BF16, int NL>
+__device__ __forceinline__ void tile_store(const GatherArgs& a, const TileHdr& h, int r, int c, bool on,
+                                           const uint4 (&w)[NL], const Quant& q, uint16_t sb, uint16_t zb) {
+  const uint32_t H = uint32_t(a.H), D = uint32_t(a.D);
+  const bool lane0 = (threadIdx.x & 63) == 0;
+  const __amdgpu_buffer_rsrc_t out = __builtin_amdgcn_make_buffer_rsrc(h.tile, 0, h.tile_bytes, 0x00020000);
+  if (h.bits == 16) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        w0 |= c[e] << (4 * e);
-        w1 |= c[8 + e] << (4 * e);
-      }
-      *reinterpret_cast<uint32_t*>(row + 4 * j) = w0;
-      *reinterpret_cast<uint32_t*>(row + D / 4 + 4 * j) = w1;
+    for (int i = 0; i < NL; ++i) {
+      const int t = i * a.rpl + r;
+      const uint32_t off = on && t < a.B ? (uint32_t(t) * H + uint32_t(h.head)) * D * 2 + 16u * uint32_t(c) : kDropOffset;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w[i]), out, off, 0, 0);
+    }
+    if (lane0) *h.scale_word = 0u;
+    return;
+  }
+  const bool flat = q.scale == 0.0;  // every value equals the zero: code 0
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int t = i * a.rpl + r;
+    const bool valid = t < h.n_valid && !flat;
+    const bool store = on && t < a.B;
+    const uint4 x = fresh(w[i]);
+    if (h.bits == 8) {
+      uint2 v = make_uint2(encode_word<BF16, 4>(make_uint4(x.x, x.y, 0, 0), q),
+                           encode_word<BF16, 4>(make_uint4(x.z, x.w, 0, 0), q));
+      v = valid ? v : make_uint2(0, 0);
+      const uint32_t off = store ? (uint32_t(t) * H + uint32_t(h.head)) * D + 8u * uint32_t(c) : kDropOffset;
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), out, off, 0, 0);
+    } else {
+      uint32_t v = encode_word<BF16, 8>(x, q);
+      v = valid ? v : 0u;
+      const uint32_t off = store ? (uint32_t(t) * H + uint32_t(h.head)) * (D / 2) + 4u * uint32_t(c) : kDropOffset;
+      __builtin_amdgcn_raw_buffer_store_b32(v, out, off, 0, 0);
     }
   }
-  if (scale_writer) {
-    *reinterpret_cast<uint32_t*>(a.scales + u.scale_off + 4 * head + 2 * which) = uint32_t(sb) | (uint32_t(zb) << 16);
+  if (lane0) *h.scale_word = uint32_t(sb) | (uint32_t(zb) << 16);
+}
+
+template <bool BF16, int NL>
+__global__ __launch_bounds__(kGatherMaxWaves * 64) void gather_tile_kernel(TileArgs s,
+                                                                             const Unit* __restrict__ units) {
+  const GatherArgs& a = s.g;
+  const int lane = threadIdx.x & 63;
+  const int r = lane / a.lpr;
+  const int c = lane - r * a.lpr;
+  const bool on = r < a.rpl;
+  const int64_t T = int64_t(blockIdx.x) * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (T >= s.num_tiles) return;
+  const TileHdr h = tile_header(a, units, T);
+  uint4 w[NL];
+  uint16_t sb, zb;
+  load_tile<NL>(a, h, r, c, w);
+  const Quant q = tile_range<BF16, NL>(a, h, r, on, w, sb, zb);
+  tile_store<BF16, NL>(a, h, r, c, on, w, q, sb, zb);
+}
+
+template <bool BF16, int NL>
+hipError_t launch_tile_nl(const TileArgs& s, const Unit* units, int wg, hipStream_t stream) {
+  const int64_t waves = wg / 64;
+  const dim3 grid(static_cast<uint32_t>((s.num_tiles + waves - 1) / waves));
+  hipLaunchKernelGGL((gather_tile_kernel<BF16, NL>), grid, dim3(wg), 0, stream, s, units);
+  return hipGetLastError();
+}
+
+template <bool BF16>
+hipError_t launch_tile(const TileArgs& s, const Unit* units, int nl, int wg, hipStream_t stream) {
+  switch (nl) {
+    case 2: return launch_tile_nl<BF16, 2>(s, units, wg, stream);
+    case 4: return launch_tile_nl<BF16, 4>(s, units, wg, stream);
+    default: return launch_tile_nl<BF16, 8>(s, units, wg, stream);
   }
 }
 
 template <bool BF16>
-__global__ __launch_bounds__(1024) void gather_kernel(GatherArgs a) {
-  __shared__ int32_t s_min[kMaxRowElems / 16];
-  __shared__ int32_t s_max[kMaxRowElems / 16];
-  const Unit u = a.units[blockIdx.x];
-  const int tid = threadIdx.x;
-  const int tag = u.tag & 0xFF;
-  const int t0 = tid / a.cols;
-  const bool active = t0 < a.tpp;
-  const int c = tid - t0 * a.cols;
-  const int dq = a.D >> 4;
-  const int head = active ? c / dq : 0;
-  const int j = active ? c - head * dq : 0;
-  for (int which = 0; which < 2; ++which) {
-    const int bits = which == 0 ? kKeyBits[tag] : kValueBits[tag];
-    if (bits != 16) {
-      for (int h = tid; h < a.H; h += blockDim.x) {
-        s_min[h] = order_key(__builtin_inff());
-        s_max[h] = order_key(-__builtin_inff());
-      }
-      __syncthreads();
-    }
-    encode_tile<BF16>(a, u, which == 0 ? a.k_cache : a.v_cache, a.payload + (which == 0 ? u.k_off : u.v_off), which,
-                      bits, s_min, s_max, active, t0, head, j);
-    __syncthreads();  // the next tile reuses the LDS range
+void launch_gather(const GatherArgs& a, int nl, dim3 grid, dim3 block, hipStream_t stream) {
+  switch (nl) {
+    case 2: hipLaunchKernelGGL((gather_kernel<BF16, 2>), grid, block, 0, stream, a); break;
+    case 4: hipLaunchKernelGGL((gather_kernel<BF16, 4>), grid, block, 0, stream, a); break;
+    case 8: hipLaunchKernelGGL((gather_kernel<BF16, 8>), grid, block, 0, stream, a); break;
+    default: hipLaunchKernelGGL((gather_kernel<BF16, 16>), grid, block, 0, stream, a); break;
   }
 }
 
@@ -297,14 +590,28 @@ pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, co
   a.D = m.head_dim;
   a.B = m.block_tokens;
   a.log2P = plan->host.log2_page;
-  a.cols = m.num_kv_heads * m.head_dim / 16;
-  a.tpp = plan->host.workgroup / a.cols;
-  const dim3 grid(static_cast<uint32_t>(info.num_units)), block(plan->host.workgroup);
+  a.lpr = m.head_dim / 8;
+  a.rpl = 64 / a.lpr;
+  const int nload = (m.block_tokens + a.rpl - 1) / a.rpl;  // loads per lane covering a block
+  const int nl = pkv::gather_loads_per_chunk(nload);
+  a.nchunk = (nload + nl - 1) / nl;
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  if (a.nchunk == 1 && nl <= 8 && m.block_tokens <= 2 * m.page_size + 1 && a.layer_elems * 2 < (int64_t(1) << 32)) {
+    // Tiles of at most 8 loads per lane on at most kUnitPages pages, layer
+    // slices below 4 GiB: the tile kernel.
+    pkv::TileArgs sa;
+    sa.g = a;
+    sa.num_tiles = info.num_units * 2 * m.num_kv_heads;
+    const hipError_t e = m.out_dtype == PKV_OUT_BF16
+                             ? pkv::launch_tile<true>(sa, plan->d_units, nl, plan->host.workgroup, stream)
+                             : pkv::launch_tile<false>(sa, plan->d_units, nl, plan->host.workgroup, stream);
+    return e == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
+  }
+  const dim3 grid(static_cast<uint32_t>(2 * info.num_units)), block(plan->host.workgroup);
   if (m.out_dtype == PKV_OUT_BF16)
-    hipLaunchKernelGGL(pkv::gather_kernel<true>, grid, block, 0, stream, a);
+    pkv::launch_gather<true>(a, nl, grid, block, stream);
   else
-    hipLaunchKernelGGL(pkv::gather_kernel<false>, grid, block, 0, stream, a);
+    pkv::launch_gather<false>(a, nl, grid, block, stream);
   return hipGetLastError() == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
 }
 

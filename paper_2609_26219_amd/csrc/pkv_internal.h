@@ -22,19 +22,24 @@ constexpr int kUnitElems = 16384;
 constexpr int kKeyBits[4] = {16, 8, 8, 4};
 constexpr int kValueBits[4] = {16, 8, 4, 4};
 
-// One workgroup's work: every head of up to `n_valid` consecutive tokens of
-// one reused block of one layer of one request.  64 bytes.
+// One work item.  Restore: every head of up to `n_valid` consecutive tokens
+// of one reused block of one layer of one request.  Checkpoint write: one
+// whole block of one layer of one request.  64 bytes.
 struct Unit {
   uint64_t k_off;      // byte offset of the unit's first K row in the payload
   uint64_t v_off;      // byte offset of its first V row
   uint64_t scale_off;  // binary16-element offset of the block's (head 0, K, scale) entry
-  int64_t row0;        // logical destination row of the unit's first token
+  int64_t row0;        // logical row of the unit's first token (destination / old context)
   int64_t pt_off;      // offset, in int32, of the request's page table
-  int32_t table_off;   // offset, in doubles, of the request's [D/2][2] (cos, sin) table
+  union {
+    int32_t table_off;  // restore: offset, in doubles, of the request's [D/2][2] (cos, sin) table
+    int32_t page0;      // checkpoint: physical page of logical page row0 >> log2(P)
+  };
   int32_t layer;
   int32_t tag;         // bits 0-7: pkv_tag_t; bit 8: rotate keys (Delta != 0)
   int32_t n_valid;     // tokens in the unit
-  int64_t reserved;
+  int32_t page1;       // checkpoint: the next two physical pages of the block's rows,
+  int32_t page2;       //   -1 past its last page; restore: 0
 };
 static_assert(sizeof(Unit) == 64, "Unit layout");
 constexpr int32_t kUnitRotate = 1 << 8;
@@ -66,11 +71,15 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
 pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoint_request_t* requests,
                                    int32_t num_requests, HostPlan* out);
 
-// Threads per workgroup of the checkpoint kernel: enough that each thread
-// holds at most kGatherTokens tokens of a block; 0 if the model needs more
-// than 1024.
-constexpr int kGatherTokens = 4;
+// Checkpoint kernel: one wave per (head, K|V) tile of a block, at most
+// kGatherMaxWaves waves per workgroup; a lane holds up to
+// gather_loads_per_chunk(n) 16-byte loads of a tile in registers.
+constexpr int kGatherMaxWaves = 16;
+// A checkpoint unit carries the block's first three source pages, enough
+// for every block when block_tokens <= 2 * page_size + 1.
+constexpr int kUnitPages = 3;
 int32_t gather_workgroup(const pkv_model_t& m);
+inline int gather_loads_per_chunk(int nload) { return nload <= 2 ? 2 : nload <= 4 ? 4 : nload <= 8 ? 8 : 16; }
 
 // The plan object behind pkv_plan_t (host metadata + one device allocation).
 }  // namespace pkv

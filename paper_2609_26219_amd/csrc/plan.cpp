@@ -186,7 +186,8 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
             u.layer = int32_t(l);
             u.tag = tag | (q.delta != 0 ? kUnitRotate : 0);
             u.n_valid = int32_t(std::min<int64_t>(per_unit, n_valid - t0));
-            u.reserved = 0;
+            u.page1 = 0;
+            u.page2 = 0;
             hp.units.push_back(u);
           }
           hp.info.restored_rows += n_valid;
@@ -205,10 +206,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
 }
 
 int32_t gather_workgroup(const pkv_model_t& m) {
-  const int64_t cols = int64_t(m.num_kv_heads) * m.head_dim / 16;
-  const int64_t rows = (m.block_tokens + kGatherTokens - 1) / kGatherTokens;
-  const int64_t threads = (cols * rows + 63) / 64 * 64;
-  return threads <= 1024 ? int32_t(threads) : 0;
+  return 64 * std::min<int32_t>(m.num_kv_heads, kGatherMaxWaves);
 }
 
 pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoint_request_t* requests,
@@ -217,7 +215,6 @@ pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoin
   if (st != PKV_OK) return st;
   if (num_requests < 0 || (num_requests > 0 && !requests) || !out) return PKV_ERR_INVALID_ARGUMENT;
   const pkv_model_t& m = *model;
-  if (gather_workgroup(m) == 0) return PKV_ERR_INVALID_ARGUMENT;
   const int64_t B = m.block_tokens, H = m.num_kv_heads, D = m.head_dim, P = m.page_size, L = m.num_layers;
   const int lp2 = ilog2(P);
   // Fields and tags.
@@ -301,11 +298,13 @@ pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoin
           u.scale_off = q.scale_offset + (uint64_t(l) * nb + b) * H * 4;
           u.row0 = q.src_row0 + b * B;
           u.pt_off = pt_off;
-          u.table_off = 0;
           u.layer = int32_t(l);
           u.tag = tag;
           u.n_valid = int32_t(std::min<int64_t>(B, q.suffix_tokens - b * B));
-          u.reserved = 0;
+          const int64_t first = u.row0 >> lp2, last = (u.row0 + u.n_valid - 1) >> lp2;
+          u.page0 = q.page_table[first];
+          u.page1 = first + 1 <= last ? q.page_table[first + 1] : -1;
+          u.page2 = first + 2 <= last ? q.page_table[first + 2] : -1;
           hp.units.push_back(u);
         }
         hp.info.bytes_written += layer_bytes + uint64_t(nb) * H * 4 * 2;

@@ -273,14 +273,22 @@ def test_checkpoint_plan_errors():
         assert _ck_status(shape, [r, reqs[1]]) == pb.PKV_ERR_INVALID_ARGUMENT, field
 
 
-def test_checkpoint_plan_workgroup_limit():
+@pytest.mark.parametrize("H,D,B", [(32, 128, 32), (2, 512, 1024), (8, 16, 4), (3, 48, 6)])
+def test_checkpoint_plan_any_valid_model(H, D, B):
+    """Every model pkv_restore_plan accepts is accepted; the workgroup is one
+    wave per head, at most 16."""
     import dataclasses
+
+    from test_gather_indexing import checkpoint_units
     shape, reqs = _ckpt_base()
-    big = dataclasses.replace(shape, num_kv_heads=32, head_dim=128, block_tokens=32)  # 256 cols x 8 rows > 1024
-    for r in reqs:
-        nb = wl.num_blocks(r.suffix_tokens, 32)
-        r.tags = np.zeros(nb, np.uint8)
-    assert _ck_status(big, reqs) == pb.PKV_ERR_INVALID_ARGUMENT
+    big = dataclasses.replace(shape, num_kv_heads=H, head_dim=D, block_tokens=B)
+    for i, r in enumerate(reqs):
+        r.tags = np.zeros(wl.num_blocks(r.suffix_tokens, B), np.uint8)
+        r.payload_offset = i << 30
+        r.scale_offset = i << 20
+    assert _ck_status(big, reqs) == VALID
+    units, wg = checkpoint_units(big, reqs)
+    assert wg == 64 * min(H, 16) and len(units) == big.num_layers * sum(len(r.tags) for r in reqs)
 
 
 def test_plan_kinds_are_not_interchangeable(lib):

@@ -24,9 +24,9 @@ def torch():
     return _t
 
 
-def _gpu_checkpoint(case, torch):
+def _gpu_checkpoint(case, torch, caches=None):
     s = case.src_shape
-    kc, vc = case.host_old_caches()
+    kc, vc = case.host_old_caches() if caches is None else caches
     dk = torch.from_numpy(kc.view(np.int16)).cuda()
     dv = torch.from_numpy(vc.view(np.int16)).cuda()
     payload = torch.full((case.payload_nbytes,), FILL, dtype=torch.uint8, device="cuda")
@@ -39,8 +39,8 @@ def _gpu_checkpoint(case, torch):
     return kc, vc, payload.cpu().numpy(), scales.cpu().numpy().view(np.uint16), info
 
 
-def _check_against_oracle(case, torch):
-    kc, vc, payload, scales, info = _gpu_checkpoint(case, torch)
+def _check_against_oracle(case, torch, caches=None):
+    kc, vc, payload, scales, info = _gpu_checkpoint(case, torch, caches)
     ref_p, ref_s = oq.quantize_gather(case.src_shape, case.requests, kc, vc, case.payload_nbytes, case.scale_elems)
     inside_p = np.zeros(case.payload_nbytes, bool)
     inside_s = np.zeros(case.scale_elems, bool)
@@ -67,10 +67,42 @@ def test_checkpoint_bit_exact_named(name, int4, torch):
     dict(L=1, H=4, D=128, B=64, P=32, n_tokens=(130,), deltas=(9,), rho0s=(31,), out_dtype=wl.OUT_BF16),
     dict(L=2, H=3, D=128, B=32, P=8, n_tokens=(70, 1, 33), deltas=(0, 2, -4), rho0s=(5, 9, 60), out_dtype=wl.OUT_FP16),
     dict(L=1, H=8, D=256, B=8, P=16, n_tokens=(41,), deltas=(3,), rho0s=(5,), out_dtype=wl.OUT_BF16),
-], ids=["bf16_two_requests", "b64_bf16", "h3_three_requests_fp16", "d256_b8"])
+    dict(L=1, H=2, D=512, B=64, P=16, n_tokens=(150,), deltas=(2,), rho0s=(9,), out_dtype=wl.OUT_BF16),
+    dict(L=2, H=20, D=16, B=8, P=8, n_tokens=(21, 50), deltas=(1, 0), rho0s=(3, 8), out_dtype=wl.OUT_FP16),
+    dict(L=1, H=3, D=48, B=16, P=16, n_tokens=(37,), deltas=(2,), rho0s=(5,), out_dtype=wl.OUT_FP16),
+    # blocks spanning more than three pages: the general kernel with 4 and 2 loads per lane
+    dict(L=1, H=4, D=64, B=32, P=8, n_tokens=(77,), deltas=(1,), rho0s=(6,), out_dtype=wl.OUT_BF16),
+    dict(L=2, H=2, D=32, B=16, P=4, n_tokens=(45, 16), deltas=(0, 3), rho0s=(2, 9), out_dtype=wl.OUT_FP16),
+], ids=["bf16_two_requests", "b64_bf16", "h3_three_requests_fp16", "d256_b8", "d512_b64_streamed_twice",
+        "h20_d16", "d48_idle_lanes", "general_nl4", "general_nl2"])
 def test_checkpoint_bit_exact_custom(params, torch):
     case = wl.make_custom(11, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), outlier_pairs=1, **params)
     _check_against_oracle(case, torch)
+
+
+@pytest.mark.parametrize("out", [wl.OUT_FP16, wl.OUT_BF16])
+def test_checkpoint_exact_and_near_ties(out, torch):
+    """Rows on a grid of half-integer multiples of the scale (exact ties, which
+    round to even) and one cache ulp either side of them: the codes must
+    equal the oracle's correctly rounded double-precision ones."""
+    case = wl.make_custom(31 + out, L=2, H=4, D=64, B=16, P=16, n_tokens=(90, 37), deltas=(3, -1), rho0s=(5, 40),
+                          tag_set=(1, 2, 3), mix=(1, 1, 1), out_dtype=out)
+    s = case.src_shape
+    kc, vc = case.host_old_caches()
+    rng = np.random.default_rng(5)
+    for cache in (kc, vc):
+        for layer in range(s.num_layers):
+            flat = cache[layer].reshape(-1, s.num_kv_heads, s.head_dim)
+            for ri in range(len(case.requests)):
+                slots = case.suffix_bits(ri, layer)[0]
+                step = 2.0 ** -int(rng.integers(2, 6))  # a binary16 scale
+                grid = (rng.integers(0, 15, size=(len(slots), s.num_kv_heads, s.head_dim)) + 0.5) * step
+                ulp = rng.choice([-1, 0, 1], size=grid.shape)
+                bits = wl.to_cache_bits(grid, out).astype(np.int32) + ulp
+                bits[:, :, 0] = wl.to_cache_bits(np.zeros(1), out)[0]   # min 0: zero 0
+                bits[:, :, 1] = wl.to_cache_bits(np.full(1, 15 * step), out)[0]  # max 15 * step
+                flat[slots] = bits.astype(np.uint16)
+    _check_against_oracle(case, torch, (kc, vc))
 
 
 def test_write_then_restore_cycle(torch):

@@ -13,12 +13,16 @@ import pytest
 from paper_2609_26219_amd import binding as pb
 from paper_2609_26219_amd import workloads as wl
 
-GATHER_TOKENS = 4  # tokens per thread
+MAX_WAVES = 16  # waves per workgroup at most
 KBITS = (16, 8, 8, 4)
 VBITS = (16, 8, 4, 4)
 UNIT_DTYPE = np.dtype([("k_off", "<u8"), ("v_off", "<u8"), ("scale_off", "<u8"), ("row0", "<i8"), ("pt_off", "<i8"),
                        ("table_off", "<i4"), ("layer", "<i4"), ("tag", "<i4"), ("n_valid", "<i4"),
-                       ("reserved", "<i8")])
+                       ("page1", "<i4"), ("page2", "<i4")])
+
+
+def loads_per_chunk(nload):
+    return 2 if nload <= 2 else 4 if nload <= 4 else 8 if nload <= 8 else 16
 
 
 def checkpoint_units(shape, requests):
@@ -38,76 +42,84 @@ def checkpoint_units(shape, requests):
 
 
 def emulate(case):
+    """Workgroup 2u + which encodes the K (0) or V (1) tile of unit u; wave w
+    of it encodes heads w, w + waves, ...; lane l holds channels
+    [8c, 8c + 8) of row r of every load (r = l // (D/8), c = l % (D/8))."""
     s = case.src_shape
     H, D, B, P, L = s.num_kv_heads, s.head_dim, s.block_tokens, s.page_size, s.num_layers
     units, WG = checkpoint_units(s, case.requests)
-    cols = H * D // 16
-    tpp = WG // cols
-    assert WG % 64 == 0 and WG <= 1024 and tpp * GATHER_TOKENS >= B
-    dq = D // 16
-    tid = np.arange(WG)
-    t0 = tid // cols
-    active = t0 < tpp
-    c = tid % cols
-    head = c // dq
-    j = c % dq
+    assert WG == 64 * min(H, MAX_WAVES)
+    nwaves = WG // 64
+    lpr = D // 8
+    rpl = 64 // lpr
+    lane = np.arange(64)
+    r, c = lane // lpr, lane % lpr
+    on = r < rpl
+    nload = -(-B // rpl)
+    NL = loads_per_chunk(nload)
+    nchunk = -(-nload // NL)
     layer_elems = s.pool_pages * P * H * D
     cache_read = np.zeros(L * layer_elems, dtype=np.int32)
     pw = np.zeros(case.payload_nbytes, dtype=np.int32)
     sw = np.zeros(case.scale_elems, dtype=np.int32)
-    pt_all = np.concatenate([r.src_page_table for r in case.requests]).astype(np.int64)
-    assert len(units) == L * sum(r.num_blocks for r in case.requests)
+    pt_all = np.concatenate([r_.src_page_table for r_ in case.requests]).astype(np.int64)
+    assert len(units) == L * sum(r_.num_blocks for r_ in case.requests)
+    passes_of = {}
     for u in units:
         tag = int(u["tag"]) & 0xFF
         n_valid = int(u["n_valid"])
         assert 1 <= n_valid <= B
         for which, (off, bits) in enumerate(((int(u["k_off"]), KBITS[tag]), (int(u["v_off"]), VBITS[tag]))):
-            for i in range(GATHER_TOKENS):
-                t = t0 + i * tpp
-                rd = active & (t < n_valid)
-                wr = active & (t < B)
-                for th in np.nonzero(rd)[0]:
-                    row = int(u["row0"]) + int(t[th])
-                    page = int(pt_all[int(u["pt_off"]) + (row // P)])
-                    assert 0 <= page < s.pool_pages
-                    base = int(u["layer"]) * layer_elems + (page * P + row % P) * H * D + int(head[th]) * D
-                    for o in (8 * int(j[th]), D // 2 + 8 * int(j[th])):
-                        assert base + o + 8 <= cache_read.size
-                        cache_read[base + o: base + o + 8] += 1
-                for th in np.nonzero(wr)[0]:
-                    r = int(t[th]) * H + int(head[th])
-                    jj = int(j[th])
-                    if bits == 16:
-                        spans = [(off + r * D * 2 + 16 * jj, 16), (off + r * D * 2 + D + 16 * jj, 16)]
-                    elif bits == 8:
-                        spans = [(off + r * D + 8 * jj, 8), (off + r * D + D // 2 + 8 * jj, 8)]
-                    else:
-                        spans = [(off + r * (D // 2) + 4 * jj, 4), (off + r * (D // 2) + D // 4 + 4 * jj, 4)]
-                    for st, ln in spans:
-                        assert 0 <= st and st + ln <= pw.size
-                        pw[st: st + ln] += 1
-            writers = np.nonzero(active & (t0 == 0) & (j == 0))[0]
-            for th in writers:
-                e = int(u["scale_off"]) + 4 * int(head[th]) + 2 * which
-                sw[e: e + 2] += 1
+            passes = 1 if bits == 16 or nchunk == 1 else 2
+            passes_of[(int(u["layer"]), int(u["row0"]), which)] = passes
+            for w in range(nwaves):
+                for head in range(w, H, nwaves):
+                    for ch in range(nchunk):
+                        for i in range(NL):
+                            t = (ch * NL + i) * rpl + r
+                            rd = on & (t < n_valid)
+                            rows = int(u["row0"]) + t[rd]
+                            pages = pt_all[int(u["pt_off"]) + rows // P]
+                            assert ((pages >= 0) & (pages < s.pool_pages)).all()
+                            base = int(u["layer"]) * layer_elems + (pages * P + rows % P) * H * D + head * D + 8 * c[rd]
+                            for e in range(8):
+                                np.add.at(cache_read, base + e, passes)
+                            wr = on & (t < B)
+                            tt, cc = t[wr], c[wr]
+                            if bits == 16:
+                                st, ln = off + (tt * H + head) * D * 2 + 16 * cc, 16
+                            elif bits == 8:
+                                st, ln = off + (tt * H + head) * D + 8 * cc, 8
+                            else:
+                                st, ln = off + (tt * H + head) * (D // 2) + 4 * cc, 4
+                            assert (st >= 0).all() and (st + ln <= pw.size).all()
+                            for b in range(ln):
+                                np.add.at(pw, st + b, 1)
+                    e0 = int(u["scale_off"]) + 4 * head + 2 * which
+                    sw[e0: e0 + 2] += 1
     # every checkpoint byte / scale element exactly once, nothing else
     want_p = np.zeros_like(pw)
     want_s = np.zeros_like(sw)
-    for r in case.requests:
-        pbytes, selems = wl.encoded_request_nbytes(case.shape, r)
-        want_p[r.payload_offset: r.payload_offset + pbytes] = 1
-        want_s[r.scale_offset: r.scale_offset + selems] = 1
+    for r_ in case.requests:
+        pbytes, selems = wl.encoded_request_nbytes(case.shape, r_)
+        want_p[r_.payload_offset: r_.payload_offset + pbytes] = 1
+        want_s[r_.scale_offset: r_.scale_offset + selems] = 1
     assert np.array_equal(pw, want_p)
     assert np.array_equal(sw, want_s)
-    # reads: exactly the suffix rows, each element of each row read once per (layer, K|V) pass
+    # reads: exactly the suffix rows, once per pass of each (layer, K|V) tile
     want_r = np.zeros_like(cache_read)
-    for r in case.requests:
-        rows = r.src_row0 + np.arange(r.suffix_tokens)
-        slots = r.src_page_table[rows // P].astype(np.int64) * P + rows % P
-        for layer in range(L):
-            for sl in slots:
-                b0 = layer * layer_elems + sl * H * D
-                want_r[b0: b0 + H * D] += 2
+    for r_ in case.requests:
+        for b in range(r_.num_blocks):
+            tag = int(r_.tags[b])
+            n = min(B, r_.suffix_tokens - b * B)
+            rows = r_.src_row0 + b * B + np.arange(n)
+            slots = r_.src_page_table[rows // P].astype(np.int64) * P + rows % P
+            for layer in range(L):
+                for which, bits in enumerate((KBITS[tag], VBITS[tag])):
+                    k = 1 if bits == 16 or nchunk == 1 else 2
+                    for sl in slots:
+                        b0 = layer * layer_elems + sl * H * D
+                        want_r[b0: b0 + H * D] += k
     assert np.array_equal(cache_read, want_r)
 
 
@@ -122,6 +134,61 @@ def emulate(case):
                            tag_set=(0, 2), mix=(1, 1)),
     lambda: wl.make_custom(5, L=2, H=8, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,),
                            tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
-], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "h4_b64", "h8_d128"])
+    # D = 48: 6 lanes per row, lanes 60..63 idle; D = 512 with B = 64: two chunks (rows streamed twice)
+    lambda: wl.make_custom(6, L=1, H=2, D=48, B=16, P=16, n_tokens=(37,), deltas=(2,), rho0s=(5,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+    lambda: wl.make_custom(7, L=1, H=2, D=512, B=64, P=16, n_tokens=(150,), deltas=(-2,), rho0s=(9,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+    lambda: wl.make_custom(8, L=1, H=20, D=16, B=8, P=8, n_tokens=(21,), deltas=(1,), rho0s=(3,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "h4_b64", "h8_d128", "d48_idle_lanes",
+        "d512_two_chunks", "h20_heads_loop"])
 def test_gather_addresses(maker):
     emulate(maker())
+
+
+@pytest.mark.parametrize("maker", [
+    lambda: wl.make_case("tiny"),
+    lambda: wl.make_custom(2, L=1, H=8, D=64, B=4, P=16, n_tokens=(23, 9), deltas=(5, 0), rho0s=(7, 40),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+    lambda: wl.make_custom(3, L=1, H=4, D=64, B=64, P=32, n_tokens=(130,), deltas=(-9,), rho0s=(31,),
+                           tag_set=(0, 2), mix=(1, 1)),
+    lambda: wl.make_custom(5, L=2, H=8, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+    lambda: wl.make_custom(8, L=1, H=20, D=16, B=8, P=8, n_tokens=(21,), deltas=(1,), rho0s=(3,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+], ids=["tiny", "h8_b4_two_requests", "h4_d64_b64", "h8_d128", "h20_heads_loop"])
+def test_tile_kernel_tiles_and_pages(maker):
+    """Tile kernel (blocks of at most 2P + 1 tokens, at most 8 loads per lane):
+    wave w of workgroup b encodes tile b * waves + w of the (unit, K|V, head)
+    order, so a grid of ceil(tiles / waves) workgroups encodes every tile
+    exactly once; the three source pages carried in each unit give every
+    valid row's page, and rows past n_valid read the block's first row."""
+    case = maker()
+    s = case.src_shape
+    H, D, B, P = s.num_kv_heads, s.head_dim, s.block_tokens, s.page_size
+    assert B <= 2 * P + 1
+    units, WG = checkpoint_units(s, case.requests)
+    nwaves = WG // 64
+    ntiles = len(units) * 2 * H
+    grid = -(-ntiles // nwaves)
+    T = (np.arange(grid)[:, None] * nwaves + np.arange(nwaves)[None, :]).reshape(-1)
+    T = T[T < ntiles]
+    assert np.array_equal(np.sort(T), np.arange(ntiles))
+    # tile -> (unit, K|V, head)
+    ui, rest = T // (2 * H), T % (2 * H)
+    assert ((rest >= H) == (rest // H == 1)).all() and (ui < len(units)).all()
+    pt_all = np.concatenate([r_.src_page_table for r_ in case.requests]).astype(np.int64)
+    lpr = D // 8
+    rpl = 64 // lpr
+    nload = -(-B // rpl)
+    assert loads_per_chunk(nload) <= 8 and loads_per_chunk(nload) >= nload
+    for u in units:
+        pages = [int(u["table_off"]), int(u["page1"]), int(u["page2"])]  # page0 shares table_off's slot
+        first = int(u["row0"]) // P
+        for t in range(B):
+            row = int(u["row0"]) + (t if t < int(u["n_valid"]) else 0)
+            k = row // P - first
+            assert 0 <= k <= 2
+            assert pages[k] == pt_all[int(u["pt_off"]) + row // P]
+            assert 0 <= pages[k] < s.pool_pages

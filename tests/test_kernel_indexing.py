@@ -23,7 +23,7 @@ VBITS = (16, 8, 4, 4)
 UNIT_ELEMS = 16384  # target output elements per unit
 UNIT_DTYPE = np.dtype([("k_off", "<u8"), ("v_off", "<u8"), ("scale_off", "<u8"), ("row0", "<i8"), ("pt_off", "<i8"),
                        ("table_off", "<i4"), ("layer", "<i4"), ("tag", "<i4"), ("n_valid", "<i4"),
-                       ("reserved", "<i8")])
+                       ("page1", "<i4"), ("page2", "<i4")])
 
 
 def host_units(shape, requests):

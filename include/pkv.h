@@ -153,6 +153,37 @@ pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* req
 pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t payload_bytes, const void* scales,
                          uint64_t scale_bytes, void* k_cache, void* v_cache, uint64_t cache_bytes, void* hip_stream);
 
+/* Streamed restore from host memory (the transport of Section IV-D and
+ * Section V-A: the checkpoint sits in CPU DRAM, copies are asynchronous from
+ * pinned memory, and only reused blocks move).  For each layer in turn, the
+ * byte ranges of that layer's reused (F) blocks and that layer's scale
+ * entries are copied host -> device, into `payload` / `scales` at the
+ * checkpoint's own offsets, on a copy stream owned by the plan; the layer's
+ * restore is then enqueued on `hip_stream` behind those copies.  Copies of
+ * layer l + 1 therefore overlap the restore of layer l.  Repair-block
+ * payload bytes cross the host link only where a repair block sits between
+ * two reused ones closer than 512 KiB apart (one copy then covers all three:
+ * cheaper than a second copy's setup); a layer's scale entries, 8 bytes per
+ * block and head, are copied whole.  The copies start only after work already
+ * enqueued on `hip_stream` (which may still read `payload`) has finished.
+ *   host_payload / host_scales : host memory holding the whole checkpoint
+ *     (>= the plan's payload_bytes / scale_bytes).  Pinned memory
+ *     (hipHostMalloc) gives asynchronous copies at link speed; pageable
+ *     memory works, but the runtime stages it and the call may block.
+ *   payload / scales : device buffers receiving the copies (as in
+ *     pkv_restore); bytes outside the copied ranges are not written.
+ *   k_cache, v_cache, cache_bytes, hip_stream : as in pkv_restore.
+ * Returns after enqueueing; everything is complete once `hip_stream` has
+ * passed the last layer.  The host buffers must stay valid until then.
+ * Calls on one plan must not overlap (they share its copy stream), and the
+ * plan must be a restore plan.  The stream and its events are created on
+ * the first call and released by pkv_free.  Errors: PKV_ERR_INVALID_ARGUMENT,
+ * PKV_ERR_DEVICE. */
+pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payload, uint64_t host_payload_bytes,
+                                   const void* host_scales, uint64_t host_scale_bytes, void* payload,
+                                   uint64_t payload_bytes, void* scales, uint64_t scale_bytes, void* k_cache,
+                                   void* v_cache, uint64_t cache_bytes, void* hip_stream);
+
 /* Release a plan and its device memory.  NULL is a no-op.  The caller must
  * make sure no enqueued restore still uses it. */
 void pkv_free(pkv_plan_t* plan);
@@ -223,6 +254,8 @@ typedef struct {
   uint64_t bytes_written;     /* output bytes, K and V */
   int32_t device;             /* HIP device the plan lives on */
   int32_t kind;               /* 0 = restore plan, 1 = checkpoint plan */
+  uint64_t host_copy_bytes;   /* restore plans: bytes pkv_restore_from_host copies (F-block ranges + scales) */
+  int64_t host_copies;        /* restore plans: number of host -> device copies it issues */
 } pkv_plan_info_t;
 
 pkv_status_t pkv_plan_query(const pkv_plan_t* plan, pkv_plan_info_t* info);

@@ -24,8 +24,8 @@ PKV_ERR_OUT_OF_MEMORY = -6
 PKV_ERR_DEVICE = -7
 
 # Every symbol include/pkv.h declares.
-EXPORTED = ("pkv_payload_size", "pkv_restore_plan", "pkv_restore", "pkv_free", "pkv_plan_query",
-            "pkv_status_string", "pkv_checkpoint_plan", "pkv_quantize_gather")
+EXPORTED = ("pkv_payload_size", "pkv_restore_plan", "pkv_restore", "pkv_restore_from_host", "pkv_free",
+            "pkv_plan_query", "pkv_status_string", "pkv_checkpoint_plan", "pkv_quantize_gather")
 
 
 class PkvModel(ctypes.Structure):
@@ -51,7 +51,8 @@ class PkvPlanInfo(ctypes.Structure):
     _fields_ = [("num_requests", ctypes.c_int64), ("num_units", ctypes.c_int64), ("restored_rows", ctypes.c_int64),
                 ("payload_bytes", ctypes.c_uint64), ("scale_bytes", ctypes.c_uint64),
                 ("cache_bytes", ctypes.c_uint64), ("bytes_read", ctypes.c_uint64),
-                ("bytes_written", ctypes.c_uint64), ("device", ctypes.c_int32), ("kind", ctypes.c_int32)]
+                ("bytes_written", ctypes.c_uint64), ("device", ctypes.c_int32), ("kind", ctypes.c_int32),
+                ("host_copy_bytes", ctypes.c_uint64), ("host_copies", ctypes.c_int64)]
 
 
 class PkvError(RuntimeError):
@@ -79,6 +80,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pkv_restore_plan.restype = i32
     lib.pkv_restore.argtypes = [vp, vp, u64, vp, u64, vp, vp, u64, vp]
     lib.pkv_restore.restype = i32
+    lib.pkv_restore_from_host.argtypes = [vp, vp, u64, vp, u64, vp, u64, vp, u64, vp, vp, u64, vp]
+    lib.pkv_restore_from_host.restype = i32
     lib.pkv_free.argtypes = [vp]
     lib.pkv_free.restype = None
     lib.pkv_plan_query.argtypes = [vp, ctypes.POINTER(PkvPlanInfo)]
@@ -250,6 +253,35 @@ def pkv_restore(plan: Plan, payload: int, payload_bytes: int, scales: int, scale
 
 def pkv_restore_status(plan: Plan, *args) -> int:
     return load().pkv_restore(plan.handle, *args)
+
+
+def pkv_restore_from_host(plan: Plan, host_payload: int, host_payload_bytes: int, host_scales: int,
+                          host_scale_bytes: int, payload: int, payload_bytes: int, scales: int, scale_bytes: int,
+                          k_cache: int, v_cache: int, cache_bytes: int, stream: int = 0) -> None:
+    """Enqueue a streamed restore from host memory; host_* are host addresses."""
+    st = load().pkv_restore_from_host(plan.handle, host_payload, host_payload_bytes, host_scales, host_scale_bytes,
+                                      payload, payload_bytes, scales, scale_bytes, k_cache, v_cache, cache_bytes,
+                                      stream or None)
+    if st != PKV_OK:
+        raise PkvError(st, "pkv_restore_from_host")
+
+
+def pkv_restore_from_host_status(plan: Plan, *args) -> int:
+    return load().pkv_restore_from_host(plan.handle, *args)
+
+
+def restore_from_host_tensors(plan: Plan, host_payload, host_scales, payload, scales, k_cache, v_cache,
+                              stream=None) -> None:
+    """Marshal torch tensors (host ones ideally pinned) into pkv_restore_from_host."""
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream(k_cache.device)
+    nbytes = lambda t: t.numel() * t.element_size()
+    pkv_restore_from_host(plan, host_payload.data_ptr(), nbytes(host_payload), host_scales.data_ptr(),
+                          nbytes(host_scales), payload.data_ptr(), nbytes(payload), scales.data_ptr(),
+                          nbytes(scales), k_cache.data_ptr(), v_cache.data_ptr(), nbytes(k_cache),
+                          stream.cuda_stream)
 
 
 def pkv_free(plan: Plan) -> None:

@@ -50,6 +50,18 @@ struct ReqInfo {
   int64_t pt_off;     // offset, in int32, of the request's page table
 };
 
+struct CopyRange {
+  uint64_t off, len;  // bytes
+};
+// Streamed restore: two copies of one layer whose ranges are at most this
+// many bytes apart are merged into one (the repair blocks between them are
+// copied too): one host -> device copy costs a fixed setup time that a gap
+// of this size takes to transfer at link speed.
+#ifndef PKV_HOST_GAP_BYTES
+#define PKV_HOST_GAP_BYTES (512u << 10)
+#endif
+constexpr uint64_t kHostGapBytes = PKV_HOST_GAP_BYTES;
+
 // Everything the plan needs on the device, built on the host.
 struct HostPlan {
   int32_t kind = 0;  // 0 = restore, 1 = checkpoint write
@@ -61,6 +73,13 @@ struct HostPlan {
   std::vector<int32_t> page_tables;
   pkv_plan_info_t info;
   int32_t log2_page;
+  // Restore plans: units are layer-major; layer l owns units
+  // [layer_units[l], layer_units[l + 1]).  Host -> device copy ranges of the
+  // streamed restore, merged, layer-major: payload bytes and scale bytes,
+  // layer l owning [*_layer[l], *_layer[l + 1]).  Kept on the host.
+  std::vector<int64_t> layer_units;
+  std::vector<CopyRange> payload_ranges, scale_ranges;
+  std::vector<int64_t> payload_layer, scale_layer;
 };
 
 // Validate and build the host side of a plan.  Makes no HIP call.
@@ -90,6 +109,11 @@ struct pkv_plan {
   double* d_tables = nullptr;
   int32_t* d_page_tables = nullptr;
   int device = -1;
+  // Streamed restore: copy stream and events (hipStream_t / hipEvent_t),
+  // created on first use.  events[0] marks the caller's stream at entry,
+  // events[1 + l] the end of layer l's copies.
+  void* copy_stream = nullptr;
+  std::vector<void*> events;
 };
 namespace pkv {
 // Copy a built host plan to device memory on the current device and wrap it.

@@ -140,6 +140,9 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
   try {
     hp.reqs.resize(num_requests);
     hp.tables.resize(size_t(num_requests) * size_t(D));
+    // Per request: page table, cos/sin table, block offsets inside a layer.
+    std::vector<std::vector<uint64_t>> block_off(num_requests);
+    std::vector<uint64_t> layer_bytes(num_requests, 0);
     for (int32_t r = 0; r < num_requests; ++r) {
       const pkv_request_t& q = requests[r];
       const int64_t nb = ceil_div(q.suffix_tokens, B);
@@ -155,20 +158,54 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
       }
       if (nb == 0) continue;
       // Block offsets inside one layer: runs by tag, ascending blocks.
-      std::vector<uint64_t> block_off(nb);
+      block_off[r].resize(nb);
       uint64_t pos = 0;
       for (int tag = 0; tag < 4; ++tag)
         for (int64_t b = 0; b < nb; ++b)
           if (q.tags[b] == tag) {
-            block_off[b] = pos;
+            block_off[r][b] = pos;
             pos += tile_bytes(m, kKeyBits[tag]) + tile_bytes(m, kValueBits[tag]);
           }
-      const uint64_t layer_bytes = pos;
-      const int64_t per_unit = unit_tokens(m);
-      hp.info.payload_bytes = std::max<uint64_t>(hp.info.payload_bytes, q.payload_offset + uint64_t(L) * layer_bytes);
+      layer_bytes[r] = pos;
+      hp.info.payload_bytes = std::max<uint64_t>(hp.info.payload_bytes, q.payload_offset + uint64_t(L) * pos);
       hp.info.scale_bytes =
           std::max<uint64_t>(hp.info.scale_bytes, (q.scale_offset + uint64_t(L) * nb * H * 4) * 2);
-      for (int64_t l = 0; l < L; ++l) {
+    }
+    // Work list, layer-major, and the streamed restore's copy ranges.
+    const int64_t per_unit = unit_tokens(m);
+    // Append a copy, merging it with the previous one (if that one is at
+    // index >= first) when it starts at most `gap` bytes after that one ends.
+    auto add_range = [](std::vector<CopyRange>& v, int64_t first, uint64_t off, uint64_t len, uint64_t gap) {
+      if (int64_t(v.size()) > first && v.back().off + v.back().len <= off &&
+          off - (v.back().off + v.back().len) <= gap)
+        v.back().len = off + len - v.back().off;
+      else
+        v.push_back(CopyRange{off, len});
+    };
+    hp.layer_units.assign(1, 0);
+    hp.payload_layer.assign(1, 0);
+    hp.scale_layer.assign(1, 0);
+    for (int64_t l = 0; l < L; ++l) {
+      for (int32_t r = 0; r < num_requests; ++r) {
+        const pkv_request_t& q = requests[r];
+        const int64_t nb = ceil_div(q.suffix_tokens, B);
+        const ReqInfo& rd = hp.reqs[r];
+        const uint64_t layer_base = q.payload_offset + uint64_t(l) * layer_bytes[r];
+        bool any_quantized = false;
+        // Payload ranges in layout order (runs by tag, ascending blocks) so
+        // that neighbouring reused blocks merge into one copy; merging stays
+        // inside this request's layer, so copies never overlap.
+        const int64_t first_range = int64_t(hp.payload_ranges.size());
+        for (int tag = 0; tag < 4; ++tag)
+          for (int64_t b = 0; b < nb; ++b)
+            if (q.tags[b] == tag && !q.repair_mask[b]) {
+              add_range(hp.payload_ranges, first_range, layer_base + block_off[r][b],
+                        tile_bytes(m, kKeyBits[tag]) + tile_bytes(m, kValueBits[tag]), kHostGapBytes);
+              any_quantized |= tag != PKV_TAG_FP16;
+            }
+        if (any_quantized)
+          add_range(hp.scale_ranges, hp.scale_layer.back(), (q.scale_offset + uint64_t(l) * nb * H * 4) * 2,
+                    uint64_t(nb) * H * 4 * 2, 0);
         for (int64_t b = 0; b < nb; ++b) {
           if (q.repair_mask[b]) continue;
           const int tag = q.tags[b];
@@ -176,7 +213,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
           // Split the block into units of at most `per_unit` tokens.
           for (int64_t t0 = 0; t0 < n_valid; t0 += per_unit) {
             Unit u;
-            const uint64_t block_base = q.payload_offset + uint64_t(l) * layer_bytes + block_off[b];
+            const uint64_t block_base = layer_base + block_off[r][b];
             u.k_off = block_base + uint64_t(t0) * H * D * kKeyBits[tag] / 8;
             u.v_off = block_base + tile_bytes(m, kKeyBits[tag]) + uint64_t(t0) * H * D * kValueBits[tag] / 8;
             u.scale_off = q.scale_offset + (uint64_t(l) * nb + b) * H * 4;
@@ -195,7 +232,13 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
           if (tag != PKV_TAG_FP16) hp.info.bytes_read += uint64_t(H) * 4 * 2;
         }
       }
+      hp.layer_units.push_back(int64_t(hp.units.size()));
+      hp.payload_layer.push_back(int64_t(hp.payload_ranges.size()));
+      hp.scale_layer.push_back(int64_t(hp.scale_ranges.size()));
     }
+    for (const CopyRange& c : hp.payload_ranges) hp.info.host_copy_bytes += c.len;
+    for (const CopyRange& c : hp.scale_ranges) hp.info.host_copy_bytes += c.len;
+    hp.info.host_copies = int64_t(hp.payload_ranges.size() + hp.scale_ranges.size());
   } catch (const std::bad_alloc&) {
     return PKV_ERR_OUT_OF_MEMORY;
   }
@@ -349,6 +392,41 @@ pkv_status_t pkv_internal_host_units(const pkv_model_t* model, const pkv_request
   *count = int64_t(hp.units.size());
   if (units_out && capacity >= *count && *count > 0)
     memcpy(units_out, hp.units.data(), hp.units.size() * sizeof(pkv::Unit));
+  return PKV_OK;
+}
+
+// Internal test hook (not part of pkv.h): the gap below which the streamed
+// restore merges two copies of one layer.
+uint64_t pkv_internal_host_gap_bytes() { return pkv::kHostGapBytes; }
+
+// Internal test hook (not part of pkv.h): the streamed restore's schedule.
+// ranges_out receives (offset, length) byte pairs, payload ranges first,
+// then scale ranges; layers_out receives [3][L + 1] starts: units, payload
+// ranges, scale ranges.  Counts are returned even when the buffers are short.
+pkv_status_t pkv_internal_stream_schedule(const pkv_model_t* model, const pkv_request_t* requests,
+                                          int32_t num_requests, uint64_t* ranges_out, int64_t capacity,
+                                          int64_t* n_payload, int64_t* n_scale, int64_t* layers_out) {
+  if (!n_payload || !n_scale || !layers_out || !model) return PKV_ERR_INVALID_ARGUMENT;
+  pkv::HostPlan hp;
+  pkv_status_t st = pkv::build_host_plan(model, requests, num_requests, &hp);
+  if (st != PKV_OK) return st;
+  *n_payload = int64_t(hp.payload_ranges.size());
+  *n_scale = int64_t(hp.scale_ranges.size());
+  const size_t L1 = size_t(model->num_layers) + 1;
+  for (size_t i = 0; i < L1; ++i) {
+    layers_out[i] = hp.layer_units[i];
+    layers_out[L1 + i] = hp.payload_layer[i];
+    layers_out[2 * L1 + i] = hp.scale_layer[i];
+  }
+  if (ranges_out && capacity >= *n_payload + *n_scale) {
+    size_t k = 0;
+    for (const auto* v : {&hp.payload_ranges, &hp.scale_ranges})
+      for (const pkv::CopyRange& c : *v) {
+        ranges_out[2 * k] = c.off;
+        ranges_out[2 * k + 1] = c.len;
+        ++k;
+      }
+  }
   return PKV_OK;
 }
 

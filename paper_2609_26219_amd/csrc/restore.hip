@@ -323,6 +323,51 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   return PKV_OK;
 }
 
+// Pointer, alignment, size and overlap checks shared by both restore entry points.
+pkv_status_t check_restore_buffers(const pkv_plan* plan, const void* payload, uint64_t payload_bytes,
+                                   const void* scales, uint64_t scale_bytes, const void* k_cache, const void* v_cache,
+                                   uint64_t cache_bytes) {
+  const pkv_plan_info_t& info = plan->host.info;
+  if (!payload || !scales || !k_cache || !v_cache) return PKV_ERR_INVALID_ARGUMENT;
+  if (reinterpret_cast<uintptr_t>(payload) % 16 || reinterpret_cast<uintptr_t>(scales) % 8 ||
+      reinterpret_cast<uintptr_t>(k_cache) % 16 || reinterpret_cast<uintptr_t>(v_cache) % 16)
+    return PKV_ERR_INVALID_ARGUMENT;
+  if (payload_bytes < info.payload_bytes || scale_bytes < info.scale_bytes || cache_bytes < info.cache_bytes)
+    return PKV_ERR_INVALID_ARGUMENT;
+  const uint64_t cb = info.cache_bytes;
+  if (ranges_overlap(k_cache, cb, v_cache, cb) || ranges_overlap(k_cache, cb, payload, info.payload_bytes) ||
+      ranges_overlap(v_cache, cb, payload, info.payload_bytes) || ranges_overlap(k_cache, cb, scales, info.scale_bytes) ||
+      ranges_overlap(v_cache, cb, scales, info.scale_bytes))
+    return PKV_ERR_INVALID_ARGUMENT;
+  return PKV_OK;
+}
+
+// Enqueue the restore kernel over units [u0, u0 + n) of the plan.
+pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const void* scales, void* k_cache,
+                            void* v_cache, int64_t u0, int64_t n, hipStream_t stream) {
+  const pkv_model_t& m = plan->host.model;
+  KernelArgs a;
+  a.units = plan->d_units + u0;
+  a.tables = plan->d_tables;
+  a.page_tables = plan->d_page_tables;
+  a.payload = static_cast<const uint8_t*>(payload);
+  a.scales = static_cast<const uint16_t*>(scales);
+  a.k_cache = static_cast<uint16_t*>(k_cache);
+  a.v_cache = static_cast<uint16_t*>(v_cache);
+  a.layer_elems = m.pool_pages * int64_t(m.page_size) * m.num_kv_heads * m.head_dim;
+  a.H = m.num_kv_heads;
+  a.D = m.head_dim;
+  a.log2P = plan->host.log2_page;
+  a.cols = m.num_kv_heads * m.head_dim / 16;
+  a.tpp = kWorkgroup / a.cols;
+  const dim3 grid(static_cast<uint32_t>(n)), block(kWorkgroup);
+  if (m.out_dtype == PKV_OUT_BF16)
+    hipLaunchKernelGGL(restore_kernel<true>, grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL(restore_kernel<false>, grid, block, 0, stream, a);
+  return hipGetLastError() == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
+}
+
 }  // namespace pkv
 
 extern "C" {
@@ -342,52 +387,84 @@ pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t p
   if (!plan || plan->host.kind != 0) return PKV_ERR_INVALID_ARGUMENT;
   const pkv_plan_info_t& info = plan->host.info;
   if (info.num_units == 0) return PKV_OK;
-  if (!payload || !scales || !k_cache || !v_cache) return PKV_ERR_INVALID_ARGUMENT;
-  if (reinterpret_cast<uintptr_t>(payload) % 16 || reinterpret_cast<uintptr_t>(scales) % 8 ||
-      reinterpret_cast<uintptr_t>(k_cache) % 16 || reinterpret_cast<uintptr_t>(v_cache) % 16)
-    return PKV_ERR_INVALID_ARGUMENT;
-  if (payload_bytes < info.payload_bytes || scale_bytes < info.scale_bytes || cache_bytes < info.cache_bytes)
-    return PKV_ERR_INVALID_ARGUMENT;
-  const uint64_t cb = info.cache_bytes;
-  if (pkv::ranges_overlap(k_cache, cb, v_cache, cb) || pkv::ranges_overlap(k_cache, cb, payload, info.payload_bytes) ||
-      pkv::ranges_overlap(v_cache, cb, payload, info.payload_bytes) ||
-      pkv::ranges_overlap(k_cache, cb, scales, info.scale_bytes) ||
-      pkv::ranges_overlap(v_cache, cb, scales, info.scale_bytes))
+  const pkv_status_t st = pkv::check_restore_buffers(plan, payload, payload_bytes, scales, scale_bytes, k_cache,
+                                                    v_cache, cache_bytes);
+  if (st != PKV_OK) return st;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
+  return pkv::launch_restore(plan, payload, scales, k_cache, v_cache, 0, info.num_units,
+                             static_cast<hipStream_t>(hip_stream));
+}
+
+pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payload, uint64_t host_payload_bytes,
+                                   const void* host_scales, uint64_t host_scale_bytes, void* payload,
+                                   uint64_t payload_bytes, void* scales, uint64_t scale_bytes, void* k_cache,
+                                   void* v_cache, uint64_t cache_bytes, void* hip_stream) {
+  if (!plan || plan->host.kind != 0) return PKV_ERR_INVALID_ARGUMENT;
+  const pkv_plan_info_t& info = plan->host.info;
+  if (info.num_units == 0) return PKV_OK;
+  pkv_status_t st = pkv::check_restore_buffers(plan, payload, payload_bytes, scales, scale_bytes, k_cache, v_cache,
+                                              cache_bytes);
+  if (st != PKV_OK) return st;
+  if (!host_payload || !host_scales || host_payload_bytes < info.payload_bytes || host_scale_bytes < info.scale_bytes)
     return PKV_ERR_INVALID_ARGUMENT;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
-
-  const pkv_model_t& m = plan->host.model;
-  pkv::KernelArgs a;
-  a.units = plan->d_units;
-  a.tables = plan->d_tables;
-  a.page_tables = plan->d_page_tables;
-  a.payload = static_cast<const uint8_t*>(payload);
-  a.scales = static_cast<const uint16_t*>(scales);
-  a.k_cache = static_cast<uint16_t*>(k_cache);
-  a.v_cache = static_cast<uint16_t*>(v_cache);
-  a.layer_elems = m.pool_pages * int64_t(m.page_size) * m.num_kv_heads * m.head_dim;
-  a.H = m.num_kv_heads;
-  a.D = m.head_dim;
-  a.log2P = plan->host.log2_page;
-  a.cols = m.num_kv_heads * m.head_dim / 16;
-  a.tpp = pkv::kWorkgroup / a.cols;
-  const dim3 grid(static_cast<uint32_t>(info.num_units)), block(pkv::kWorkgroup);
+  pkv_plan* p = const_cast<pkv_plan*>(plan);  // the copy stream and events are created on first use
+  const int64_t L = plan->host.model.num_layers;
+  if (!p->copy_stream) {
+    hipStream_t cs = nullptr;
+    if (hipStreamCreateWithFlags(&cs, hipStreamNonBlocking) != hipSuccess) return PKV_ERR_DEVICE;
+    p->copy_stream = cs;
+    p->events.assign(size_t(L + 1), nullptr);
+    for (auto& e : p->events) {
+      hipEvent_t ev = nullptr;
+      if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return PKV_ERR_DEVICE;
+      e = ev;
+    }
+  }
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  if (m.out_dtype == PKV_OUT_BF16)
-    hipLaunchKernelGGL(pkv::restore_kernel<true>, grid, block, 0, stream, a);
-  else
-    hipLaunchKernelGGL(pkv::restore_kernel<false>, grid, block, 0, stream, a);
-  return hipGetLastError() == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
+  hipStream_t copy = static_cast<hipStream_t>(p->copy_stream);
+  auto ev = [&](int64_t i) { return static_cast<hipEvent_t>(p->events[size_t(i)]); };
+  // Earlier work on the caller's stream may still read `payload`.
+  if (hipEventRecord(ev(0), stream) != hipSuccess || hipStreamWaitEvent(copy, ev(0), 0) != hipSuccess)
+    return PKV_ERR_DEVICE;
+  const uint8_t* hp_bytes = static_cast<const uint8_t*>(host_payload);
+  const uint8_t* hs_bytes = static_cast<const uint8_t*>(host_scales);
+  uint8_t* dp_bytes = static_cast<uint8_t*>(payload);
+  uint8_t* ds_bytes = static_cast<uint8_t*>(scales);
+  const pkv::HostPlan& h = plan->host;
+  for (int64_t l = 0; l < L; ++l) {
+    for (int64_t i = h.payload_layer[l]; i < h.payload_layer[l + 1]; ++i) {
+      const pkv::CopyRange& c = h.payload_ranges[size_t(i)];
+      if (hipMemcpyAsync(dp_bytes + c.off, hp_bytes + c.off, c.len, hipMemcpyHostToDevice, copy) != hipSuccess)
+        return PKV_ERR_DEVICE;
+    }
+    for (int64_t i = h.scale_layer[l]; i < h.scale_layer[l + 1]; ++i) {
+      const pkv::CopyRange& c = h.scale_ranges[size_t(i)];
+      if (hipMemcpyAsync(ds_bytes + c.off, hs_bytes + c.off, c.len, hipMemcpyHostToDevice, copy) != hipSuccess)
+        return PKV_ERR_DEVICE;
+    }
+    if (hipEventRecord(ev(1 + l), copy) != hipSuccess || hipStreamWaitEvent(stream, ev(1 + l), 0) != hipSuccess)
+      return PKV_ERR_DEVICE;
+    const int64_t u0 = h.layer_units[l], n = h.layer_units[l + 1] - u0;
+    if (n == 0) continue;
+    st = pkv::launch_restore(plan, payload, scales, k_cache, v_cache, u0, n, stream);
+    if (st != PKV_OK) return st;
+  }
+  return PKV_OK;
 }
 
 void pkv_free(pkv_plan_t* plan) {
   if (!plan) return;
-  if (plan->device_mem) {
+  if (plan->device_mem || plan->copy_stream) {
     int cur = -1;
     const bool switched = hipGetDevice(&cur) == hipSuccess && cur != plan->device &&
                           hipSetDevice(plan->device) == hipSuccess;
-    (void)hipFree(plan->device_mem);
+    for (void* e : plan->events)
+      if (e) (void)hipEventDestroy(static_cast<hipEvent_t>(e));
+    if (plan->copy_stream) (void)hipStreamDestroy(static_cast<hipStream_t>(plan->copy_stream));
+    if (plan->device_mem) (void)hipFree(plan->device_mem);
     if (switched) (void)hipSetDevice(cur);
   }
   delete plan;

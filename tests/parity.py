@@ -242,3 +242,63 @@ def check_sampled(dr, refs, check_untouched: bool = True) -> Stats:
         log(f"  untouched check over {s.num_layers} layers: {bad} mismatches")
         assert bad == 0
     return st
+
+
+def host_gap_bytes() -> int:
+    import ctypes
+
+    from paper_2609_26219_amd import binding as pb
+
+    fn = pb.load().pkv_internal_host_gap_bytes
+    fn.restype = ctypes.c_uint64
+    return int(fn())
+
+
+def streamed_payload_ranges(case, gap: int):
+    """Per layer, the (offset, length) payload copies a streamed restore
+    issues: every reused block's K and V tiles, requests in order, blocks in
+    layout order (runs by tag, ascending), a copy extended over a following
+    one of the same request that starts at most `gap` bytes after it ends."""
+    s = case.shape
+    B, H, D, L = s.block_tokens, s.num_kv_heads, s.head_dim, s.num_layers
+    out = []
+    for layer in range(L):
+        ranges = []
+        for ri, req in enumerate(case.requests):
+            offsets, _ = oracle.block_layout(req.tags, B, H, D)
+            base = case.layer_payload_offset(ri, layer)
+            first = len(ranges)
+            for tag in range(4):
+                for b in range(len(req.tags)):
+                    if int(req.tags[b]) != tag or req.repair[b]:
+                        continue
+                    k0, v0 = offsets[b]
+                    off, end = base + k0, base + v0 + B * H * D * oracle.VALUE_BITS[tag] // 8
+                    if len(ranges) > first and ranges[-1][1] <= off and off - ranges[-1][1] <= gap:
+                        ranges[-1][1] = end
+                    else:
+                        ranges.append([off, end])
+        out.append([(a, e - a) for a, e in ranges])
+    return out
+
+
+def reused_byte_masks(case, gap: int = 0):
+    """Boolean masks over the payload bytes and the scale elements that a
+    streamed restore copies: every reused block's K and V tiles in every
+    layer (plus repair blocks inside gaps of at most `gap` bytes), and the
+    whole per-layer scale block of each request that has a reused quantized
+    block in that layer."""
+    s = case.shape
+    H, L = s.num_kv_heads, s.num_layers
+    pmask = np.zeros(case.payload_nbytes, bool)
+    smask = np.zeros(case.scale_elems, bool)
+    for layer_ranges in streamed_payload_ranges(case, gap):
+        for off, ln in layer_ranges:
+            pmask[off: off + ln] = True
+    for ri, req in enumerate(case.requests):
+        nb = len(req.tags)
+        for layer in range(L):
+            if any(not req.repair[b] and int(req.tags[b]) != 0 for b in range(nb)):
+                so = case.layer_scale_offset(ri, layer)
+                smask[so: so + nb * H * 4] = True
+    return pmask, smask

@@ -158,7 +158,7 @@ pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t p
  * pinned memory, and only reused blocks move).  For each layer in turn, the
  * byte ranges of that layer's reused (F) blocks and that layer's scale
  * entries are copied host -> device, into `payload` / `scales` at the
- * checkpoint's own offsets, on a copy stream owned by the plan; the layer's
+ * checkpoint's own offsets, on copy streams owned by the plan; the layer's
  * restore is then enqueued on `hip_stream` behind those copies.  Copies of
  * layer l + 1 therefore overlap the restore of layer l.  Repair-block
  * payload bytes cross the host link only where a repair block sits between
@@ -175,8 +175,8 @@ pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t p
  *   k_cache, v_cache, cache_bytes, hip_stream : as in pkv_restore.
  * Returns after enqueueing; everything is complete once `hip_stream` has
  * passed the last layer.  The host buffers must stay valid until then.
- * Calls on one plan must not overlap (they share its copy stream), and the
- * plan must be a restore plan.  The stream and its events are created on
+ * Calls on one plan must not overlap (they share its copy streams), and the
+ * plan must be a restore plan.  The streams and events are created on
  * the first call and released by pkv_free.  Errors: PKV_ERR_INVALID_ARGUMENT,
  * PKV_ERR_DEVICE. */
 pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payload, uint64_t host_payload_bytes,

@@ -61,6 +61,13 @@ struct CopyRange {
 #define PKV_HOST_GAP_BYTES (512u << 10)
 #endif
 constexpr uint64_t kHostGapBytes = PKV_HOST_GAP_BYTES;
+// Streamed restore: copy streams that layers alternate between (two keep
+// the host link busier than one: 31.6 ms against 33.0 ms on the 8B-shaped
+// 32-layer checkpoint; four measured no better than two).
+#ifndef PKV_HOST_COPY_STREAMS
+#define PKV_HOST_COPY_STREAMS 2
+#endif
+constexpr int kHostCopyStreams = PKV_HOST_COPY_STREAMS;
 
 // Everything the plan needs on the device, built on the host.
 struct HostPlan {
@@ -109,10 +116,11 @@ struct pkv_plan {
   double* d_tables = nullptr;
   int32_t* d_page_tables = nullptr;
   int device = -1;
-  // Streamed restore: copy stream and events (hipStream_t / hipEvent_t),
-  // created on first use.  events[0] marks the caller's stream at entry,
-  // events[1 + l] the end of layer l's copies.
-  void* copy_stream = nullptr;
+  // Streamed restore: copy streams and events (hipStream_t / hipEvent_t),
+  // created on first use.  Layer l's copies go to copy_streams[l % n];
+  // events[0] marks the caller's stream at entry, events[1 + l] the end of
+  // layer l's copies.
+  std::vector<void*> copy_streams;
   std::vector<void*> events;
 };
 namespace pkv {

@@ -410,25 +410,38 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
     return PKV_ERR_INVALID_ARGUMENT;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
-  pkv_plan* p = const_cast<pkv_plan*>(plan);  // the copy stream and events are created on first use
+  pkv_plan* p = const_cast<pkv_plan*>(plan);  // the copy streams and events are created on first use
   const int64_t L = plan->host.model.num_layers;
-  if (!p->copy_stream) {
-    hipStream_t cs = nullptr;
-    if (hipStreamCreateWithFlags(&cs, hipStreamNonBlocking) != hipSuccess) return PKV_ERR_DEVICE;
-    p->copy_stream = cs;
-    p->events.assign(size_t(L + 1), nullptr);
-    for (auto& e : p->events) {
-      hipEvent_t ev = nullptr;
-      if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return PKV_ERR_DEVICE;
-      e = ev;
+  if (p->copy_streams.empty()) {  // all or nothing
+    std::vector<void*> streams, events;
+    bool ok = true;
+    for (int i = 0; ok && i < pkv::kHostCopyStreams; ++i) {
+      hipStream_t cs = nullptr;
+      ok = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking) == hipSuccess;
+      if (ok) streams.push_back(cs);
     }
+    for (int64_t i = 0; ok && i <= L; ++i) {
+      hipEvent_t e = nullptr;
+      ok = hipEventCreateWithFlags(&e, hipEventDisableTiming) == hipSuccess;
+      if (ok) events.push_back(e);
+    }
+    if (!ok) {
+      for (void* e : events) (void)hipEventDestroy(static_cast<hipEvent_t>(e));
+      for (void* cs : streams) (void)hipStreamDestroy(static_cast<hipStream_t>(cs));
+      return PKV_ERR_DEVICE;
+    }
+    p->copy_streams = std::move(streams);
+    p->events = std::move(events);
   }
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  hipStream_t copy = static_cast<hipStream_t>(p->copy_stream);
+  const size_t n_copy = p->copy_streams.size();
+  auto copy_stream = [&](int64_t l) { return static_cast<hipStream_t>(p->copy_streams[size_t(l) % n_copy]); };
   auto ev = [&](int64_t i) { return static_cast<hipEvent_t>(p->events[size_t(i)]); };
   // Earlier work on the caller's stream may still read `payload`.
-  if (hipEventRecord(ev(0), stream) != hipSuccess || hipStreamWaitEvent(copy, ev(0), 0) != hipSuccess)
-    return PKV_ERR_DEVICE;
+  if (hipEventRecord(ev(0), stream) != hipSuccess) return PKV_ERR_DEVICE;
+  for (size_t i = 0; i < n_copy; ++i)
+    if (hipStreamWaitEvent(static_cast<hipStream_t>(p->copy_streams[i]), ev(0), 0) != hipSuccess)
+      return PKV_ERR_DEVICE;
   const uint8_t* hp_bytes = static_cast<const uint8_t*>(host_payload);
   const uint8_t* hs_bytes = static_cast<const uint8_t*>(host_scales);
   uint8_t* dp_bytes = static_cast<uint8_t*>(payload);
@@ -437,15 +450,18 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
   for (int64_t l = 0; l < L; ++l) {
     for (int64_t i = h.payload_layer[l]; i < h.payload_layer[l + 1]; ++i) {
       const pkv::CopyRange& c = h.payload_ranges[size_t(i)];
-      if (hipMemcpyAsync(dp_bytes + c.off, hp_bytes + c.off, c.len, hipMemcpyHostToDevice, copy) != hipSuccess)
+      if (hipMemcpyAsync(dp_bytes + c.off, hp_bytes + c.off, c.len, hipMemcpyHostToDevice, copy_stream(l)) !=
+          hipSuccess)
         return PKV_ERR_DEVICE;
     }
     for (int64_t i = h.scale_layer[l]; i < h.scale_layer[l + 1]; ++i) {
       const pkv::CopyRange& c = h.scale_ranges[size_t(i)];
-      if (hipMemcpyAsync(ds_bytes + c.off, hs_bytes + c.off, c.len, hipMemcpyHostToDevice, copy) != hipSuccess)
+      if (hipMemcpyAsync(ds_bytes + c.off, hs_bytes + c.off, c.len, hipMemcpyHostToDevice, copy_stream(l)) !=
+          hipSuccess)
         return PKV_ERR_DEVICE;
     }
-    if (hipEventRecord(ev(1 + l), copy) != hipSuccess || hipStreamWaitEvent(stream, ev(1 + l), 0) != hipSuccess)
+    if (hipEventRecord(ev(1 + l), copy_stream(l)) != hipSuccess ||
+        hipStreamWaitEvent(stream, ev(1 + l), 0) != hipSuccess)
       return PKV_ERR_DEVICE;
     const int64_t u0 = h.layer_units[l], n = h.layer_units[l + 1] - u0;
     if (n == 0) continue;
@@ -457,13 +473,13 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
 
 void pkv_free(pkv_plan_t* plan) {
   if (!plan) return;
-  if (plan->device_mem || plan->copy_stream) {
+  if (plan->device_mem || !plan->copy_streams.empty()) {
     int cur = -1;
     const bool switched = hipGetDevice(&cur) == hipSuccess && cur != plan->device &&
                           hipSetDevice(plan->device) == hipSuccess;
     for (void* e : plan->events)
       if (e) (void)hipEventDestroy(static_cast<hipEvent_t>(e));
-    if (plan->copy_stream) (void)hipStreamDestroy(static_cast<hipStream_t>(plan->copy_stream));
+    for (void* cs : plan->copy_streams) (void)hipStreamDestroy(static_cast<hipStream_t>(cs));
     if (plan->device_mem) (void)hipFree(plan->device_mem);
     if (switched) (void)hipSetDevice(cur);
   }

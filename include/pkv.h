@@ -83,13 +83,26 @@ typedef enum {
 
 typedef enum { PKV_OUT_FP16 = 0, PKV_OUT_BF16 = 1 } pkv_out_dtype_t;
 
+/* Which key channels form a rotary pair (the model-aware RoPE correction of
+ * Section IV-D: the Delta rotation of Eq. 3 must use the model's own RoPE).
+ * Only the first rotary_dim channels rotate; the rest pass through.
+ *   PKV_ROPE_HALF:        pair (i, i + rotary_dim/2), i < rotary_dim/2 (Llama, Qwen, NeoX);
+ *   PKV_ROPE_INTERLEAVED: pair (2i, 2i + 1), i < rotary_dim/2 (GPT-J, GLM).
+ * Pair i turns by Delta * f_i with f_i = inv_freq[i], or rope_theta^(-2i/rotary_dim)
+ * when inv_freq is NULL. */
+typedef enum { PKV_ROPE_HALF = 0, PKV_ROPE_INTERLEAVED = 1 } pkv_rope_style_t;
+
 /* Model and cache geometry, shared by all requests of a plan.
  * Constraints (else PKV_ERR_INVALID_ARGUMENT):
  *   num_layers >= 1; 1 <= num_kv_heads; head_dim % 16 == 0, 16 <= head_dim <= 512;
  *   num_kv_heads * head_dim <= 4096; 1 <= block_tokens <= 1024;
  *   (block_tokens * num_kv_heads * head_dim) % 32 == 0 (every tile 16-byte aligned);
  *   page_size a power of two in [1, 2^20]; pool_pages >= 1;
- *   rope_theta finite and > 0; out_dtype a pkv_out_dtype_t value. */
+ *   rope_theta finite and > 0; out_dtype a pkv_out_dtype_t value;
+ *   rope_style a pkv_rope_style_t value; rotary_dim 0 (= head_dim) or a
+ *   multiple of 16 in [16, head_dim]; inv_freq NULL or rotary_dim/2 finite
+ *   values (copied at plan time).  A zero-initialised tail gives full
+ *   rotate-half RoPE with rope_theta frequencies. */
 typedef struct {
   int32_t num_layers;   /* L */
   int32_t num_kv_heads; /* H */
@@ -99,6 +112,9 @@ typedef struct {
   int32_t out_dtype;    /* pkv_out_dtype_t of k_cache / v_cache */
   int64_t pool_pages;   /* pages per layer in each cache */
   double rope_theta;    /* RoPE base */
+  int32_t rope_style;   /* pkv_rope_style_t */
+  int32_t rotary_dim;   /* rotated channels per head; 0 = head_dim */
+  const double* inv_freq; /* host [rotary_dim/2] pair frequencies, or NULL for rope_theta^(-2i/rotary_dim) */
 } pkv_model_t;
 
 /* One resumed request (one aligned suffix S).  Host arrays are copied by

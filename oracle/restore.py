@@ -27,8 +27,11 @@ recomputed elsewhere and never touched here), and every KV head:
    (the old-to-new token map of Section IV-D); nothing else is written.
 
 Readings where the paper is silent (each is listed with its reason in the
-design notes): rotate-half pairing ``(i, i + D/2)`` with frequencies
-``theta^(-2i/D)``; rotation skipped when ``Delta == 0``; tiles are token-major
+design notes): the model's own RoPE (the paper calls the correction
+model-aware): rotate-half pairs ``(i, i + R/2)`` or interleaved pairs
+``(2i, 2i + 1)`` over the first ``R`` channels, frequencies
+``theta^(-2i/R)`` unless the model gives its own table, and channels past
+``R`` untouched; rotation skipped when ``Delta == 0``; tiles are token-major
 ``[B][H][D]``; 4-bit codes put channel ``2j`` in the low nibble.
 
 Objects passed in only need the attributes used below (``Shape`` /
@@ -131,27 +134,68 @@ def decode_block(payload: np.ndarray, scales: np.ndarray, shape, req, layer: int
 # Step 3: RoPE phase correction of keys (Eq. 2, Eq. 3)
 # --------------------------------------------------------------------------
 
-def rope_angles(position: float, theta: float, D: int) -> np.ndarray:
-    """Angle of rotary pair ``i`` at a position: ``position * theta^(-2i/D)``."""
-    i = np.arange(D // 2, dtype=np.float64)
-    return position * theta ** (-2.0 * i / D)
+ROPE_HALF, ROPE_INTERLEAVED = 0, 1
 
 
-def rotate(x: np.ndarray, angles: np.ndarray) -> np.ndarray:
-    """Apply ``R`` to the last axis: pair ``(i, i + D/2)`` turns by ``angles[i]``
-    counter-clockwise."""
-    half = x.shape[-1] // 2
-    lo, hi = x[..., :half], x[..., half:]
+def rope_frequencies(theta: float, rotary_dim: int, inv_freq=None) -> np.ndarray:
+    """Frequency of rotary pair ``i < rotary_dim/2``: the given table, else
+    ``theta^(-2i/rotary_dim)``."""
+    if inv_freq is not None:
+        f = np.asarray(inv_freq, dtype=np.float64)
+        assert f.shape == (rotary_dim // 2,)
+        return f
+    i = np.arange(rotary_dim // 2, dtype=np.float64)
+    return theta ** (-2.0 * i / rotary_dim)
+
+
+def rope_angles(position: float, theta: float, D: int, inv_freq=None) -> np.ndarray:
+    """Angle of rotary pair ``i`` at a position: ``position * f_i``."""
+    return position * rope_frequencies(theta, D, inv_freq)
+
+
+def rope_pairs(D: int, rotary_dim: int, style: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Channel indices (first, second) of every rotary pair ``i``:
+    rotate-half ``(i, i + R/2)`` or interleaved ``(2i, 2i + 1)``, R = rotary_dim."""
+    i = np.arange(rotary_dim // 2)
+    if style == ROPE_HALF:
+        return i, i + rotary_dim // 2
+    if style == ROPE_INTERLEAVED:
+        return 2 * i, 2 * i + 1
+    raise ValueError(style)
+
+
+def rotate(x: np.ndarray, angles: np.ndarray, style: int = ROPE_HALF, rotary_dim: Optional[int] = None) -> np.ndarray:
+    """Apply ``R`` to the last axis: pair ``i`` (by ``style``) turns by
+    ``angles[i]`` counter-clockwise; channels from ``rotary_dim`` on are
+    returned unchanged."""
+    D = x.shape[-1]
+    R = D if rotary_dim is None else rotary_dim
+    a, b = rope_pairs(D, R, style)
     c, s = np.cos(angles), np.sin(angles)
-    return np.concatenate([lo * c - hi * s, hi * c + lo * s], axis=-1)
+    out = np.array(x, dtype=np.float64, copy=True)
+    xa, xb = x[..., a], x[..., b]
+    out[..., a] = xa * c - xb * s
+    out[..., b] = xb * c + xa * s
+    return out
 
 
-def correct_key_phase(k_old: np.ndarray, delta: int, theta: float) -> np.ndarray:
-    """``R(rho) R(omega)^-1 K_old = R(rho - omega) K_old = R(Delta) K_old``.
-    ``R(0)`` is the identity, so no arithmetic is applied when ``Delta == 0``."""
+def correct_key_phase(k_old: np.ndarray, delta: int, theta: float, style: int = ROPE_HALF,
+                      rotary_dim: Optional[int] = None, inv_freq=None) -> np.ndarray:
+    """``R(rho) R(omega)^-1 K_old = R(rho - omega) K_old = R(Delta) K_old``
+    with the model's pairing, rotated channels and frequencies.  ``R(0)`` is
+    the identity, so no arithmetic is applied when ``Delta == 0``."""
     if delta == 0:
         return k_old.copy()
-    return rotate(k_old, rope_angles(delta, theta, k_old.shape[-1]))
+    D = k_old.shape[-1]
+    R = D if not rotary_dim else rotary_dim
+    return rotate(k_old, delta * rope_frequencies(theta, R, inv_freq), style, R)
+
+
+def shape_rope(shape) -> Tuple[int, Optional[int], object]:
+    """(style, rotary_dim or None, inv_freq or None) of a shape; absent
+    attributes mean full rotate-half RoPE with theta frequencies."""
+    return (int(getattr(shape, "rope_style", ROPE_HALF)), int(getattr(shape, "rotary_dim", 0)) or None,
+            getattr(shape, "inv_freq", None))
 
 
 # --------------------------------------------------------------------------
@@ -228,7 +272,8 @@ def restore_block(payload, scales, shape, req, layer: int, block: int, layout=No
     """(slots [n], K exact fp64 [n, H, D], V exact fp64 [n, H, D]) of one reused block."""
     n = valid_tokens(req, shape.block_tokens, block)
     k_old, v = decode_block(payload, scales, shape, req, layer, block, layout)
-    k = correct_key_phase(k_old[:n], int(req.delta), float(shape.rope_theta))
+    style, rdim, inv = shape_rope(shape)
+    k = correct_key_phase(k_old[:n], int(req.delta), float(shape.rope_theta), style, rdim, inv)
     return destination_slots(shape, req, block), k, v[:n]
 
 

@@ -31,7 +31,8 @@ EXPORTED = ("pkv_payload_size", "pkv_restore_plan", "pkv_restore", "pkv_restore_
 class PkvModel(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("block_tokens", ctypes.c_int32), ("page_size", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
-                ("pool_pages", ctypes.c_int64), ("rope_theta", ctypes.c_double)]
+                ("pool_pages", ctypes.c_int64), ("rope_theta", ctypes.c_double), ("rope_style", ctypes.c_int32),
+                ("rotary_dim", ctypes.c_int32), ("inv_freq", ctypes.c_void_p)]
 
 
 class PkvRequest(ctypes.Structure):
@@ -102,9 +103,17 @@ def pkv_status_string(status: int) -> str:
 
 
 def make_model(shape) -> PkvModel:
-    """PkvModel from any object with the pkv_model_t field names."""
-    return PkvModel(int(shape.num_layers), int(shape.num_kv_heads), int(shape.head_dim), int(shape.block_tokens),
-                    int(shape.page_size), int(shape.out_dtype), int(shape.pool_pages), float(shape.rope_theta))
+    """PkvModel from any object with the pkv_model_t field names (the RoPE
+    fields are optional).  The returned structure keeps the frequency array
+    it points to alive."""
+    inv = getattr(shape, "inv_freq", None)
+    freq = None if inv is None else np.ascontiguousarray(inv, dtype=np.float64)
+    m = PkvModel(int(shape.num_layers), int(shape.num_kv_heads), int(shape.head_dim), int(shape.block_tokens),
+                 int(shape.page_size), int(shape.out_dtype), int(shape.pool_pages), float(shape.rope_theta),
+                 int(getattr(shape, "rope_style", 0)), int(getattr(shape, "rotary_dim", 0)),
+                 freq.ctypes.data if freq is not None and freq.size else None)
+    m.keep = freq
+    return m
 
 
 class _Requests:

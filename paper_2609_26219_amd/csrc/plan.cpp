@@ -38,10 +38,40 @@ pkv_status_t check_model(const pkv_model_t* m) {
   if (m->pool_pages < 1) return PKV_ERR_INVALID_ARGUMENT;
   if (!(isfinite(m->rope_theta) && m->rope_theta > 0.0)) return PKV_ERR_INVALID_ARGUMENT;
   if (m->out_dtype != PKV_OUT_FP16 && m->out_dtype != PKV_OUT_BF16) return PKV_ERR_INVALID_ARGUMENT;
+  if (m->rope_style != PKV_ROPE_HALF && m->rope_style != PKV_ROPE_INTERLEAVED) return PKV_ERR_INVALID_ARGUMENT;
+  if (m->rotary_dim != 0 && (m->rotary_dim < 16 || m->rotary_dim > m->head_dim || m->rotary_dim % 16 != 0))
+    return PKV_ERR_INVALID_ARGUMENT;
+  if (m->inv_freq) {
+    const int32_t R = m->rotary_dim ? m->rotary_dim : m->head_dim;
+    for (int32_t i = 0; i < R / 2; ++i)
+      if (!isfinite(m->inv_freq[i])) return PKV_ERR_INVALID_ARGUMENT;
+  }
   // Cache elements per layer and in total must stay far from int64 overflow.
   const double elems = double(m->num_layers) * double(m->pool_pages) * m->page_size * m->num_kv_heads * m->head_dim;
   if (elems > 1e18) return PKV_ERR_INVALID_ARGUMENT;
   return PKV_OK;
+}
+
+// RoPE helpers: rotated channels per head, the frequency of pair i, and the
+// pair that element e of key piece j rotates (k = 8j + e; -1 = none).
+int32_t rotary_dim(const pkv_model_t& m) { return m.rotary_dim ? m.rotary_dim : m.head_dim; }
+
+double rope_frequency(const pkv_model_t& m, int64_t i) {
+  const int32_t R = rotary_dim(m);
+  return m.inv_freq ? m.inv_freq[i] : pow(m.rope_theta, -2.0 * double(i) / double(R));
+}
+
+int64_t rope_table_pair(const pkv_model_t& m, int64_t k) {
+  const int64_t D = m.head_dim, R = rotary_dim(m);
+  const int64_t j = k / 8, e = k % 8;
+  if (m.rope_style == PKV_ROPE_HALF) {
+    // Piece j < R/16 holds channels [8j, 8j+8) and [R/2 + 8j, ...): pairs 8j + e.
+    return 8 * j < R / 2 ? 8 * j + e : -1;
+  }
+  // Interleaved: piece j holds channels [8j, 8j+8) (elements 0..3 are its four
+  // pairs) and [D/2 + 8j, ...) (elements 4..7); a pair rotates if inside [0, R).
+  const int64_t first = e < 4 ? 8 * j : D / 2 + 8 * j;
+  return first + 8 <= R ? first / 2 + e % 4 : -1;
 }
 
 pkv_status_t check_request_fields(const pkv_request_t& r) {
@@ -150,11 +180,14 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
       rd.table_off = int64_t(r) * D;
       rd.pt_off = int64_t(hp.page_tables.size());
       hp.page_tables.insert(hp.page_tables.end(), q.page_table, q.page_table + q.num_logical_pages);
-      // cos / sin of Delta * theta^(-2i/D), in double precision.
-      for (int64_t i = 0; i < D / 2; ++i) {
-        const double ang = double(q.delta) * pow(m.rope_theta, -2.0 * double(i) / double(D));
-        hp.tables[size_t(r) * D + 2 * i] = q.delta ? cos(ang) : 1.0;
-        hp.tables[size_t(r) * D + 2 * i + 1] = q.delta ? sin(ang) : 0.0;
+      // cos / sin of Delta * f_i in double precision, laid out in the
+      // kernel's element order: entry 8j + e is the pair that element e of
+      // key piece j rotates (rope_table_pair); pass-through entries are (1, 0).
+      for (int64_t k = 0; k < D / 2; ++k) {
+        const int64_t i = rope_table_pair(m, k);
+        const double ang = i >= 0 ? double(q.delta) * rope_frequency(m, i) : 0.0;
+        hp.tables[size_t(r) * D + 2 * k] = q.delta && i >= 0 ? cos(ang) : 1.0;
+        hp.tables[size_t(r) * D + 2 * k + 1] = q.delta && i >= 0 ? sin(ang) : 0.0;
       }
       if (nb == 0) continue;
       // Block offsets inside one layer: runs by tag, ascending blocks.
@@ -392,6 +425,19 @@ pkv_status_t pkv_internal_host_units(const pkv_model_t* model, const pkv_request
   *count = int64_t(hp.units.size());
   if (units_out && capacity >= *count && *count > 0)
     memcpy(units_out, hp.units.data(), hp.units.size() * sizeof(pkv::Unit));
+  return PKV_OK;
+}
+
+// Internal test hook (not part of pkv.h): the (cos, sin) tables of a restore
+// plan, [num_requests][D/2][2] in the kernel's element order.
+pkv_status_t pkv_internal_host_tables(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
+                                      double* out, int64_t capacity, int64_t* count) {
+  if (!count) return PKV_ERR_INVALID_ARGUMENT;
+  pkv::HostPlan hp;
+  pkv_status_t st = pkv::build_host_plan(model, requests, num_requests, &hp);
+  if (st != PKV_OK) return st;
+  *count = int64_t(hp.tables.size());
+  if (out && capacity >= *count && *count > 0) memcpy(out, hp.tables.data(), hp.tables.size() * sizeof(double));
   return PKV_OK;
 }
 

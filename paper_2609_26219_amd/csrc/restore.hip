@@ -50,6 +50,7 @@ struct KernelArgs {
   uint16_t* v_cache;
   int64_t layer_elems;  // pool_pages * P * H * D
   int32_t H, D, log2P, cols, tpp;
+  int32_t R;            // rotary channels per head
 };
 
 __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
@@ -137,13 +138,69 @@ __device__ __forceinline__ double decode_d(const Chunk8<BITS>& c, int e, double 
   }
 }
 
-// Keys of one (token, head): piece j = channels [8j, 8j+8) and [D/2+8j, ...).
-template <int KBITS, bool ROT, bool BF16>
-__device__ __forceinline__ void restore_key_piece(const uint8_t* __restrict__ row, int j, int D, float ks, float kz,
-                                                  const double2* __restrict__ cs, uint16_t* __restrict__ dst) {
+// Key piece j of a head: two runs of 8 channels, at `lo` and `hi`, and
+// whether each run rotates.  Rotate-half (pairs (i, i + R/2)): piece j < R/16
+// holds channels [8j, 8j+8) and [R/2 + 8j, ...), element e pairing with
+// element e; pieces past R/16 hold pass-through channels [R, D) in the same
+// two-halves arrangement.  Interleaved (pairs (2i, 2i+1)): piece j holds
+// [8j, 8j+8) and [D/2 + 8j, ...), each pairing elements 2k and 2k+1; a run
+// rotates when it lies inside [0, R).  The (cos, sin) table is laid out by
+// the planner in the same element order.
+struct KeyPiece {
+  int lo, hi;
+  bool rot_lo, rot_hi;
+};
+
+template <int STYLE>
+__device__ __forceinline__ KeyPiece key_piece(int j, int D, int R) {
+  KeyPiece p;
+  if constexpr (STYLE == PKV_ROPE_HALF) {
+    if (8 * j < R / 2) {
+      p.lo = 8 * j;
+      p.hi = R / 2 + 8 * j;
+      p.rot_lo = p.rot_hi = true;
+    } else {
+      const int q = j - R / 16;
+      p.lo = R + 8 * q;
+      p.hi = R + (D - R) / 2 + 8 * q;
+      p.rot_lo = p.rot_hi = false;
+    }
+  } else {
+    p.lo = 8 * j;
+    p.hi = D / 2 + 8 * j;
+    p.rot_lo = p.lo + 8 <= R;
+    p.rot_hi = p.hi + 8 <= R;
+  }
+  return p;
+}
+
+// Rotate one interleaved run: pairs (2k, 2k+1) with cs[k].
+template <int KBITS>
+__device__ __forceinline__ void rotate_pairs(const Chunk8<KBITS>& c, double s64, double z64,
+                                             const double2* __restrict__ cs, float* out) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const double x = decode_d<KBITS>(c, 2 * k, s64, z64);
+    const double y = decode_d<KBITS>(c, 2 * k + 1, s64, z64);
+    out[2 * k] = to_float(__builtin_fma(x, cs[k].x, -(y * cs[k].y)));
+    out[2 * k + 1] = to_float(__builtin_fma(y, cs[k].x, x * cs[k].y));
+  }
+}
+
+template <int KBITS>
+__device__ __forceinline__ void decode_run(const Chunk8<KBITS>& c, float s, float z, float* out) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) out[e] = decode_f<KBITS>(c, e, s, z);
+}
+
+// Keys of one (token, head), piece p.
+template <int KBITS, bool ROT, int STYLE, bool BF16>
+__device__ __forceinline__ void restore_key_piece(const uint8_t* __restrict__ row, const KeyPiece& p, float ks,
+                                                  float kz, const double2* __restrict__ cs,
+                                                  uint16_t* __restrict__ dst) {
   Chunk8<KBITS> lo, hi;
-  lo.load(row + (8 * j) * KBITS / 8);
-  hi.load(row + (D / 2 + 8 * j) * KBITS / 8);
+  lo.load(row + p.lo * KBITS / 8);
+  hi.load(row + p.hi * KBITS / 8);
   uint4 out_lo, out_hi;
   if constexpr (KBITS == 16 && !ROT && !BF16) {
     // binary16 in, binary16 out, no rotation: the bits are the result.
@@ -151,27 +208,38 @@ __device__ __forceinline__ void restore_key_piece(const uint8_t* __restrict__ ro
     out_hi = hi.w;
   } else {
     float a[8], b[8];
-    if constexpr (ROT) {
-      const double s64 = ks, z64 = kz;
+    if constexpr (ROT && STYLE == PKV_ROPE_HALF) {
+      if (p.rot_lo) {
+        const double s64 = ks, z64 = kz;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const double x = decode_d<KBITS>(lo, e, s64, z64);
-        const double y = decode_d<KBITS>(hi, e, s64, z64);
-        a[e] = to_float(__builtin_fma(x, cs[e].x, -(y * cs[e].y)));
-        b[e] = to_float(__builtin_fma(y, cs[e].x, x * cs[e].y));
+        for (int e = 0; e < 8; ++e) {
+          const double x = decode_d<KBITS>(lo, e, s64, z64);
+          const double y = decode_d<KBITS>(hi, e, s64, z64);
+          a[e] = to_float(__builtin_fma(x, cs[e].x, -(y * cs[e].y)));
+          b[e] = to_float(__builtin_fma(y, cs[e].x, x * cs[e].y));
+        }
+      } else {
+        decode_run<KBITS>(lo, ks, kz, a);
+        decode_run<KBITS>(hi, ks, kz, b);
       }
+    } else if constexpr (ROT) {  // interleaved
+      if (p.rot_lo)
+        rotate_pairs<KBITS>(lo, ks, kz, cs, a);
+      else
+        decode_run<KBITS>(lo, ks, kz, a);
+      if (p.rot_hi)
+        rotate_pairs<KBITS>(hi, ks, kz, cs + 4, b);
+      else
+        decode_run<KBITS>(hi, ks, kz, b);
     } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        a[e] = decode_f<KBITS>(lo, e, ks, kz);
-        b[e] = decode_f<KBITS>(hi, e, ks, kz);
-      }
+      decode_run<KBITS>(lo, ks, kz, a);
+      decode_run<KBITS>(hi, ks, kz, b);
     }
     out_lo = pack8<BF16>(a);
     out_hi = pack8<BF16>(b);
   }
-  store_row_piece(dst + 8 * j, out_lo);
-  store_row_piece(dst + D / 2 + 8 * j, out_hi);
+  store_row_piece(dst + p.lo, out_lo);
+  store_row_piece(dst + p.hi, out_hi);
 }
 
 // Values of one (token, head): the same piece j; never rotated.
@@ -199,7 +267,7 @@ __device__ __forceinline__ void restore_value_piece(const uint8_t* __restrict__ 
   store_row_piece(dst + D / 2 + 8 * j, out_hi);
 }
 
-template <int TAG, bool ROT, bool BF16>
+template <int TAG, bool ROT, int STYLE, bool BF16>
 __device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u, const double* __restrict__ s_tab,
                                              int t0, int head, int j) {
   constexpr int KB = kKeyBits[TAG];
@@ -224,17 +292,18 @@ __device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u,
   const int64_t slot_mask = (int64_t(1) << a.log2P) - 1;
   const int64_t row_elems = int64_t(H) * D;
   const int64_t lbase = int64_t(u.layer) * a.layer_elems + int64_t(head) * D;
+  const KeyPiece kp = key_piece<STYLE>(j, D, a.R);
   for (int t = t0; t < u.n_valid; t += a.tpp) {
     const int64_t row = u.row0 + t;
     const int64_t page = a.page_tables[u.pt_off + (row >> a.log2P)];
     const int64_t dst = lbase + ((page << a.log2P) | (row & slot_mask)) * row_elems;
     const int64_t r = int64_t(t) * H + head;
-    restore_key_piece<KB, ROT, BF16>(kbase + r * krow_bytes, j, D, ks, kz, cs, a.k_cache + dst);
+    restore_key_piece<KB, ROT, STYLE, BF16>(kbase + r * krow_bytes, kp, ks, kz, cs, a.k_cache + dst);
     restore_value_piece<VB, BF16>(vbase + r * vrow_bytes, j, D, vs, vz, a.v_cache + dst);
   }
 }
 
-template <bool BF16>
+template <bool BF16, int STYLE>
 __global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(KernelArgs a) {
   __shared__ __attribute__((aligned(16))) double s_tab[kMaxHeadDim];
   const Unit u = a.units[blockIdx.x];
@@ -252,14 +321,14 @@ __global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(Ker
   const int head = c / dq;
   const int j = c - head * dq;
   switch (tag * 2 + (rot ? 1 : 0)) {
-    case 0: restore_unit<PKV_TAG_FP16, false, BF16>(a, u, s_tab, t0, head, j); break;
-    case 1: restore_unit<PKV_TAG_FP16, true, BF16>(a, u, s_tab, t0, head, j); break;
-    case 2: restore_unit<PKV_TAG_K8V8, false, BF16>(a, u, s_tab, t0, head, j); break;
-    case 3: restore_unit<PKV_TAG_K8V8, true, BF16>(a, u, s_tab, t0, head, j); break;
-    case 4: restore_unit<PKV_TAG_K8V4, false, BF16>(a, u, s_tab, t0, head, j); break;
-    case 5: restore_unit<PKV_TAG_K8V4, true, BF16>(a, u, s_tab, t0, head, j); break;
-    case 6: restore_unit<PKV_TAG_K4V4, false, BF16>(a, u, s_tab, t0, head, j); break;
-    default: restore_unit<PKV_TAG_K4V4, true, BF16>(a, u, s_tab, t0, head, j); break;
+    case 0: restore_unit<PKV_TAG_FP16, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
+    case 1: restore_unit<PKV_TAG_FP16, true, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
+    case 2: restore_unit<PKV_TAG_K8V8, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
+    case 3: restore_unit<PKV_TAG_K8V8, true, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
+    case 4: restore_unit<PKV_TAG_K8V4, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
+    case 5: restore_unit<PKV_TAG_K8V4, true, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
+    case 6: restore_unit<PKV_TAG_K4V4, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
+    default: restore_unit<PKV_TAG_K4V4, true, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
   }
 }
 
@@ -360,11 +429,17 @@ pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const voi
   a.log2P = plan->host.log2_page;
   a.cols = m.num_kv_heads * m.head_dim / 16;
   a.tpp = kWorkgroup / a.cols;
+  a.R = m.rotary_dim ? m.rotary_dim : m.head_dim;
   const dim3 grid(static_cast<uint32_t>(n)), block(kWorkgroup);
-  if (m.out_dtype == PKV_OUT_BF16)
-    hipLaunchKernelGGL(restore_kernel<true>, grid, block, 0, stream, a);
+  const bool bf16 = m.out_dtype == PKV_OUT_BF16, half = m.rope_style == PKV_ROPE_HALF;
+  if (bf16 && half)
+    hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_HALF>), grid, block, 0, stream, a);
+  else if (bf16)
+    hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_INTERLEAVED>), grid, block, 0, stream, a);
+  else if (half)
+    hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_HALF>), grid, block, 0, stream, a);
   else
-    hipLaunchKernelGGL(restore_kernel<false>, grid, block, 0, stream, a);
+    hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_INTERLEAVED>), grid, block, 0, stream, a);
   return hipGetLastError() == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
 }
 

@@ -31,6 +31,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 import numpy as np
 
 TAG_FP16, TAG_K8V8, TAG_K8V4, TAG_K4V4 = 0, 1, 2, 3
+ROPE_HALF, ROPE_INTERLEAVED = 0, 1
 TAG_NAMES = ("FP16", "K8V8", "K8V4", "K4V4")
 KEY_BITS = (16, 8, 8, 4)
 VALUE_BITS = (16, 8, 4, 4)
@@ -41,7 +42,8 @@ FP16_NAN_BITS = 0x7E00
 # Seed streams (spawn keys) so every piece can be regenerated in isolation.
 _STREAM_TAGS, _STREAM_REPAIR, _STREAM_PAGES, _STREAM_POS, _STREAM_K, _STREAM_V = range(6)
 
-CONFIG_NAMES = ("tiny", "llama8b_1l", "llama8b_32l", "llama70b", "batched16")
+CONFIG_NAMES = ("tiny", "llama8b_1l", "llama8b_32l", "llama70b", "batched16", "qwen3_32b_1l", "glm4_9b_1l",
+                "llama33_70b_1l")
 BASE_SEED = 26090
 
 
@@ -57,6 +59,9 @@ class Shape:
     pool_pages: int
     rope_theta: float
     out_dtype: int  # OUT_FP16 or OUT_BF16
+    rope_style: int = 0  # ROPE_HALF or ROPE_INTERLEAVED
+    rotary_dim: int = 0  # 0 = head_dim
+    inv_freq: Optional[Tuple[float, ...]] = None  # explicit pair frequencies, else theta^(-2i/rotary_dim)
 
     @property
     def pool_slots(self) -> int:
@@ -388,6 +393,33 @@ def private_page_table(rng: np.random.Generator, rows_end: int, page_size: int, 
     return rng.choice(pool, size=nlp, replace=False).astype(np.int32), pool
 
 
+def llama3_inv_freq(theta: float, dim: int, factor: float = 8.0, low_freq_factor: float = 1.0,
+                    high_freq_factor: float = 4.0, original_max_position: int = 8192) -> Tuple[float, ...]:
+    """Rotary frequencies with Llama-3's published long-context scaling (a
+    model-configuration input): pairs whose wavelength is below
+    original/high_freq_factor keep theta^(-2i/dim), those above
+    original/low_freq_factor are divided by `factor`, and the band between
+    is a linear blend in original/wavelength."""
+    base = theta ** (-np.arange(0, dim, 2, dtype=np.float64) / dim)
+    wavelen = 2 * math.pi / base
+    low_wl = original_max_position / low_freq_factor
+    high_wl = original_max_position / high_freq_factor
+    smooth = (original_max_position / wavelen - low_freq_factor) / (high_freq_factor - low_freq_factor)
+    blended = (1 - smooth) * base / factor + smooth * base
+    out = np.where(wavelen < high_wl, base, np.where(wavelen > low_wl, base / factor, blended))
+    return tuple(float(x) for x in out)
+
+
+# Public architecture facts of the paper's model families (KV heads, head
+# dim, RoPE), at one layer and an 8K-token suffix.
+MODEL_ROPE = {
+    # name: (num_kv_heads, head_dim, theta, rope_style, rotary_dim, scaled frequencies)
+    "qwen3_32b_1l": (8, 128, 1.0e6, ROPE_HALF, 0, False),
+    "glm4_9b_1l": (2, 128, 1.0e4, ROPE_INTERLEAVED, 64, False),
+    "llama33_70b_1l": (8, 128, 5.0e5, ROPE_HALF, 0, True),
+}
+
+
 def make_case(name: str, seed: Optional[int] = None, distinct_layers: Optional[int] = None,
               int4_tag: int = TAG_K8V4) -> Case:
     """One of the five named workloads (see ``CONFIG_NAMES``)."""
@@ -426,6 +458,19 @@ def make_case(name: str, seed: Optional[int] = None, distinct_layers: Optional[i
         return Case(name, shape, [req], seed, distinct_layers or L, outlier_pairs=1)
     if name == "batched16":
         return make_batched(seed, distinct_layers=distinct_layers or 2, int4_tag=int4_tag)
+    if name in MODEL_ROPE:
+        H, D, theta, style, rdim, scaled = MODEL_ROPE[name]
+        B, P, N = 32, 16, 8192
+        nb = num_blocks(N, B)
+        tags = draw_tags(g(_STREAM_TAGS), nb, (0.7, 0.2, 0.1), int4_tag)
+        repair = draw_repair_edit_local(g(_STREAM_REPAIR), nb, 0.10)
+        delta = int(g(_STREAM_POS).integers(-4096, 4097))
+        rho0 = draw_positions(_rng(seed, _STREAM_POS, 1), delta)
+        pt, pool = private_page_table(g(_STREAM_PAGES), rho0 + N, P)
+        inv = llama3_inv_freq(theta, D) if scaled else None
+        shape = Shape(1, H, D, B, P, pool, theta, OUT_BF16, style, rdim, inv)
+        req = Request(N, delta, rho0, tags, repair, pt)
+        return Case(name, shape, [req], seed, distinct_layers or 1, outlier_pairs=1)
     raise ValueError(name)
 
 

@@ -59,6 +59,40 @@ def test_property_cases(params, torch):
     check_full(*restore_small(case))
 
 
+@pytest.mark.parametrize("name", ["qwen3_32b_1l", "glm4_9b_1l", "llama33_70b_1l"])
+def test_model_family_rope(name, torch):
+    """The paper's model families with their own RoPE: Qwen3 (rotate-half,
+    theta 1e6), GLM-4 (interleaved pairs on half the head), Llama-3.3
+    (rotate-half with scaled frequencies)."""
+    log(f"[gpu] {name}: full-cache parity with the model's RoPE")
+    st = check_full(*restore_small(wl.make_case(name)))
+    log(f"  {st}")
+    assert st.bit_exact_fraction > 0.9999
+
+
+ROPE_CASES = [
+    # (D, rotary_dim, style, scaled frequencies, tag set, out dtype)
+    (128, 64, wl.ROPE_HALF, False, (0, 1, 2, 3), wl.OUT_BF16),
+    (128, 32, wl.ROPE_INTERLEAVED, True, (0, 2), wl.OUT_FP16),
+    (64, 64, wl.ROPE_INTERLEAVED, False, (1, 3), wl.OUT_BF16),
+    (256, 96, wl.ROPE_HALF, True, (0, 1, 2), wl.OUT_FP16),
+    (48, 16, wl.ROPE_INTERLEAVED, False, (0, 1, 2, 3), wl.OUT_BF16),
+]
+
+
+@pytest.mark.parametrize("params", ROPE_CASES, ids=[f"rope{i}" for i in range(len(ROPE_CASES))])
+def test_rope_variant_cases(params, torch):
+    import dataclasses
+    D, R, style, scaled, tags, out = params
+    case = wl.make_custom(50 + len(tags), L=2, H=3, D=D, B=16, P=16, n_tokens=(70, 33), deltas=(-2049, 5),
+                          rho0s=(2100, 9), tag_set=tags, mix=[1.0] * len(tags), repair_frac=0.2, out_dtype=out,
+                          outlier_pairs=1)
+    case.shape = dataclasses.replace(case.shape, rope_style=style, rotary_dim=0 if R == D else R,
+                                     inv_freq=wl.llama3_inv_freq(5e5, R) if scaled else None)
+    log(f"[gpu] rope variant {params}")
+    check_full(*restore_small(case))
+
+
 def test_all_repair_writes_nothing(torch):
     case = wl.make_custom(21, L=2, n_tokens=(64, 20), deltas=(4, 2), repair_all=True)
     dr, _ = restore_small(case)

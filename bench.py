@@ -180,6 +180,18 @@ def host_restore(torch, binding, dr, steps: int, stream):
     torch.cuda.synchronize()
     ms = sorted(a.elapsed_time(b) for a, b in ev)
     avg = sum(ms) / len(ms)
+    # zero-copy: the restore kernel reads the pinned checkpoint directly
+    zc = lambda: binding.restore_tensors(dr.plan, hp, hs, dr.k_cache, dr.v_cache, stream)
+    zc()
+    torch.cuda.synchronize()
+    zev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in zev:
+        a.record(stream)
+        zc()
+        b.record(stream)
+    torch.cuda.synchronize()
+    zms = sorted(a.elapsed_time(b) for a, b in zev)
+    zavg = sum(zms) / len(zms)
     # practical ceiling: one pinned host -> device copy of the same byte count
     n = int(info["host_copy_bytes"])
     dst = torch.empty(n, dtype=torch.uint8, device="cuda")
@@ -197,8 +209,10 @@ def host_restore(torch, binding, dr, steps: int, stream):
     need = int(info["bytes_read"])  # reused blocks' payload and scales: what must cross the link
     achieved = need / (avg * 1e-3) / 1e9
     full = dr.payload.numel() + 2 * dr.scales.numel()
+    zachieved = need / (zavg * 1e-3) / 1e9
     log(f"[bench] streamed restore from host: {avg:.2f} ms, {n / (avg * 1e-3) / 1e9:.1f} GB/s copied over the host "
-        f"link, {achieved:.1f} GB/s of reused-block bytes (one plain pinned copy of the same bytes: {copy_gbps:.1f} GB/s)")
+        f"link, {achieved:.1f} GB/s of reused-block bytes (one plain pinned copy of the same bytes: {copy_gbps:.1f} GB/s); "
+        f"zero-copy restore {zavg:.2f} ms, {zachieved:.1f} GB/s")
     return {
         "what": "pkv_restore_from_host: per layer, reused blocks' payload ranges and the layer's scales copied "
                 "from pinned host memory on a copy stream, each layer's restore enqueued behind its copies",
@@ -219,8 +233,66 @@ def host_restore(torch, binding, dr, steps: int, stream):
             "traffic": None,
         },
         "plain_pinned_copy_GBps": round(copy_gbps, 2),
+        "zero_copy": {
+            "what": "pkv_restore with the checkpoint in pinned host memory: the kernel reads only the reused "
+                    "blocks over the host link, one launch",
+            "ms": round(zavg, 3),
+            "ms_p10_p50_p90": [round(zms[int(q * (len(zms) - 1))], 3) for q in (0.1, 0.5, 0.9)],
+            "GBps": round(zachieved, 2),
+            "frac_of_pcie_peak": round(zachieved / PCIE_PEAK_GBPS, 4),
+        },
         "copied_frac_of_plain_copy": round(n / (avg * 1e-3) / 1e9 / copy_gbps, 4),
     }
+
+
+REPRESENTATIONS = (("FP16", 0), ("INT8 (K8V8)", 1), ("K8V4", 2), ("INT4 (K4V4)", 3), ("mixed (workload tags)", None))
+
+
+def representations(torch, binding, wl, case, old, steps: int, host_steps: int, stream):
+    """The representation axis of the transport ablation: the same suffix,
+    repair set and old caches, checkpointed uniformly in one representation
+    (or with the workload's per-block tags), then restored from HBM and
+    streamed from pinned host memory."""
+    import dataclasses
+
+    import numpy as np
+
+    from paper_2609_26219_amd.device import DeviceCheckpoint, DeviceRestore
+
+    rows = []
+    for label, tag in REPRESENTATIONS:
+        reqs = [dataclasses.replace(r, tags=np.full_like(r.tags, tag)) if tag is not None else r
+                for r in case.requests]
+        c = wl.Case(case.name, case.shape, [dataclasses.replace(r) for r in reqs], case.seed, case.distinct_layers,
+                    case.outlier_pairs)
+        ck = DeviceCheckpoint(c, old)
+        ck.write(stream)
+        torch.cuda.synchronize()
+        dr = DeviceRestore(c, checkpoint=(ck.payload, ck.scales))
+        del ck
+        info = dr.info
+        nbytes = info["bytes_read"] + info["bytes_written"]
+        ms, _ = time_launches(torch, lambda i: dr.run(stream), steps, 2, stream)
+        avg = sum(ms) / len(ms)
+        host = host_restore(torch, binding, dr, host_steps, stream)
+        rows.append({
+            "representation": label,
+            "checkpoint_bytes": int(c.payload_nbytes + 2 * c.scale_elems),
+            "restore_bytes_read": int(info["bytes_read"]),
+            "restore_us": round(avg * 1e3, 1),
+            "restore_GBps": round(nbytes / (avg * 1e-3) / 1e9, 1),
+            "pct_hbm_peak": round(100 * nbytes / (avg * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+            "from_host_ms": host["fetch_and_dequant_ms"],
+            "from_host_GBps": host["roofline"]["achieved"],
+            "zero_copy_ms": host["zero_copy"]["ms"],
+            "zero_copy_GBps": host["zero_copy"]["GBps"],
+        })
+        log(f"[bench] {label}: checkpoint {rows[-1]['checkpoint_bytes'] / 2**20:.1f} MiB, restore "
+            f"{rows[-1]['restore_us']} us ({rows[-1]['pct_hbm_peak']}% HBM), from host {rows[-1]['from_host_ms']} ms "
+            f"(DMA), {rows[-1]['zero_copy_ms']} ms (zero-copy)")
+        del dr
+        torch.cuda.empty_cache()
+    return rows
 
 
 def copy_reference(torch, nbytes: int = 4 << 30, reps: int = 10):
@@ -252,6 +324,8 @@ def main():
     ap.add_argument("--sets", type=int, default=2, help="buffer sets cycled between steps")
     ap.add_argument("--write-steps", type=int, default=10, help="timed checkpoint-write launches")
     ap.add_argument("--host-steps", type=int, default=5, help="timed streamed restores from pinned host memory")
+    ap.add_argument("--no-representations", action="store_true",
+                    help="skip the uniform-representation comparison (FP16 / K8V8 / K8V4 / K4V4 / mixed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ref", action="store_true")
     args = ap.parse_args()
@@ -287,8 +361,6 @@ def main():
     w_achieved = w_bytes / (w_avg * 1e-3) / 1e9
     log(f"[bench] checkpoint write avg {w_avg * 1e3:.1f} us, {w_achieved:.0f} GB/s")
     ck.old = None
-    del old
-    torch.cuda.empty_cache()
 
     sets = [DeviceRestore(case, checkpoint=(ck.payload, ck.scales)) for _ in range(max(1, args.sets))]
     del ck
@@ -365,6 +437,13 @@ def main():
     }
     if args.host_steps > 0:
         out["host_restore"] = host_restore(torch, binding, sets[0], args.host_steps, stream)
+    if not args.no_representations:
+        del sets[1:]
+        torch.cuda.empty_cache()
+        out["representations"] = representations(torch, binding, wl, case, old, 10, max(1, min(args.host_steps, 3)),
+                                                  stream)
+    del old
+    torch.cuda.empty_cache()
     if not args.no_copy_ref:
         del sets
         torch.cuda.empty_cache()

@@ -156,10 +156,15 @@ pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* req
 
 /* Enqueue the restore described by `plan` on `hip_stream` (a hipStream_t;
  * NULL = the default stream) and return without waiting.
- *   payload      : device, >= the plan's payload_bytes (pkv_plan_query), 16-byte aligned;
- *   scales       : device binary16, >= the plan's scale_bytes, 8-byte aligned;
- *   k_cache/v_cache : device, each cache_bytes = L*pool_pages*P*H*D*2, 16-byte aligned,
- *                  must not overlap each other or the inputs;
+ *   payload      : >= the plan's payload_bytes (pkv_plan_query), 16-byte aligned;
+ *   scales       : binary16, >= the plan's scale_bytes, 8-byte aligned;
+ *     either may be device memory or pinned host memory (hipHostMalloc,
+ *     which is mapped for the device): the kernel then reads the checkpoint
+ *     over the host link (a zero-copy restore: only the reused blocks'
+ *     bytes cross it, in one launch).  Pageable host memory and another
+ *     device's memory are PKV_ERR_INVALID_ARGUMENT;
+ *   k_cache/v_cache : device memory of the plan's device, each cache_bytes =
+ *                  L*pool_pages*P*H*D*2, 16-byte aligned, must not overlap each other or the inputs;
  *   *_bytes      : the caller's allocation sizes, checked against what the plan reads / writes.
  * The current device must be the plan's device.  All buffers must stay alive
  * until the stream has passed the restore.  Calls that share a plan are safe
@@ -271,7 +276,7 @@ typedef struct {
   int32_t device;             /* HIP device the plan lives on */
   int32_t kind;               /* 0 = restore plan, 1 = checkpoint plan */
   uint64_t host_copy_bytes;   /* restore plans: bytes pkv_restore_from_host copies (F-block ranges + scales) */
-  int64_t host_copies;        /* restore plans: number of host -> device copies it issues */
+  int64_t host_copies;        /* restore plans: number of host -> device copies it issues (after chunking) */
 } pkv_plan_info_t;
 
 pkv_status_t pkv_plan_query(const pkv_plan_t* plan, pkv_plan_info_t* info);

@@ -271,7 +271,8 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
     }
     for (const CopyRange& c : hp.payload_ranges) hp.info.host_copy_bytes += c.len;
     for (const CopyRange& c : hp.scale_ranges) hp.info.host_copy_bytes += c.len;
-    hp.info.host_copies = int64_t(hp.payload_ranges.size() + hp.scale_ranges.size());
+    for (const auto* v : {&hp.payload_ranges, &hp.scale_ranges})
+      for (const CopyRange& c : *v) hp.info.host_copies += int64_t((c.len + kHostChunkBytes - 1) / kHostChunkBytes);
   } catch (const std::bad_alloc&) {
     return PKV_ERR_OUT_OF_MEMORY;
   }

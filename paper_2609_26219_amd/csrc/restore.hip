@@ -392,6 +392,39 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   return PKV_OK;
 }
 
+// Where the kernel may read an input from: device or managed memory of the
+// plan's device as is; pinned host memory through its device mapping (the
+// kernel then reads it over the host link).  Pageable host memory, or memory
+// of another device, is rejected: the kernel would fault on it.
+pkv_status_t kernel_readable(const pkv_plan* plan, const void* p, const void** out) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return PKV_ERR_INVALID_ARGUMENT;
+  }
+  if ((a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged) && a.device == plan->device) {
+    *out = p;
+    return PKV_OK;
+  }
+  if (a.type == hipMemoryTypeHost && a.devicePointer) {
+    *out = a.devicePointer;
+    return PKV_OK;
+  }
+  return PKV_ERR_INVALID_ARGUMENT;
+}
+
+// Caches must be device (or managed) memory of the plan's device.
+pkv_status_t device_writable(const pkv_plan* plan, const void* p) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return PKV_ERR_INVALID_ARGUMENT;
+  }
+  return (a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged) && a.device == plan->device
+             ? PKV_OK
+             : PKV_ERR_INVALID_ARGUMENT;
+}
+
 // Pointer, alignment, size and overlap checks shared by both restore entry points.
 pkv_status_t check_restore_buffers(const pkv_plan* plan, const void* payload, uint64_t payload_bytes,
                                    const void* scales, uint64_t scale_bytes, const void* k_cache, const void* v_cache,
@@ -462,12 +495,17 @@ pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t p
   if (!plan || plan->host.kind != 0) return PKV_ERR_INVALID_ARGUMENT;
   const pkv_plan_info_t& info = plan->host.info;
   if (info.num_units == 0) return PKV_OK;
-  const pkv_status_t st = pkv::check_restore_buffers(plan, payload, payload_bytes, scales, scale_bytes, k_cache,
-                                                    v_cache, cache_bytes);
+  pkv_status_t st = pkv::check_restore_buffers(plan, payload, payload_bytes, scales, scale_bytes, k_cache, v_cache,
+                                              cache_bytes);
   if (st != PKV_OK) return st;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
-  return pkv::launch_restore(plan, payload, scales, k_cache, v_cache, 0, info.num_units,
+  const void *p_dev = nullptr, *s_dev = nullptr;
+  if ((st = pkv::kernel_readable(plan, payload, &p_dev)) != PKV_OK ||
+      (st = pkv::kernel_readable(plan, scales, &s_dev)) != PKV_OK || (st = pkv::device_writable(plan, k_cache)) != PKV_OK ||
+      (st = pkv::device_writable(plan, v_cache)) != PKV_OK)
+    return st;
+  return pkv::launch_restore(plan, p_dev, s_dev, k_cache, v_cache, 0, info.num_units,
                              static_cast<hipStream_t>(hip_stream));
 }
 
@@ -485,6 +523,9 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
     return PKV_ERR_INVALID_ARGUMENT;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
+  if ((st = pkv::device_writable(plan, payload)) != PKV_OK || (st = pkv::device_writable(plan, scales)) != PKV_OK ||
+      (st = pkv::device_writable(plan, k_cache)) != PKV_OK || (st = pkv::device_writable(plan, v_cache)) != PKV_OK)
+    return st;
   pkv_plan* p = const_cast<pkv_plan*>(plan);  // the copy streams and events are created on first use
   const int64_t L = plan->host.model.num_layers;
   if (p->copy_streams.empty()) {  // all or nothing
@@ -495,7 +536,7 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
       ok = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking) == hipSuccess;
       if (ok) streams.push_back(cs);
     }
-    for (int64_t i = 0; ok && i <= L; ++i) {
+    for (int64_t i = 0; ok && i < 1 + L * pkv::kHostCopyStreams; ++i) {
       hipEvent_t e = nullptr;
       ok = hipEventCreateWithFlags(&e, hipEventDisableTiming) == hipSuccess;
       if (ok) events.push_back(e);
@@ -510,7 +551,6 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
   }
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   const size_t n_copy = p->copy_streams.size();
-  auto copy_stream = [&](int64_t l) { return static_cast<hipStream_t>(p->copy_streams[size_t(l) % n_copy]); };
   auto ev = [&](int64_t i) { return static_cast<hipEvent_t>(p->events[size_t(i)]); };
   // Earlier work on the caller's stream may still read `payload`.
   if (hipEventRecord(ev(0), stream) != hipSuccess) return PKV_ERR_DEVICE;
@@ -522,22 +562,35 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
   uint8_t* dp_bytes = static_cast<uint8_t*>(payload);
   uint8_t* ds_bytes = static_cast<uint8_t*>(scales);
   const pkv::HostPlan& h = plan->host;
+  // Copies are cut into chunks of at most kHostChunkBytes and dealt to the
+  // copy streams in turn, so every stream (each feeding its own DMA engine)
+  // stays busy within a layer; layer l's restore waits on every stream that
+  // carried one of its chunks.
+  size_t next = 0;
+  auto enqueue = [&](uint8_t* dst, const uint8_t* src, const pkv::CopyRange& c, uint32_t& used) {
+    for (uint64_t o = 0; o < c.len; o += pkv::kHostChunkBytes) {
+      const uint64_t n = c.len - o < pkv::kHostChunkBytes ? c.len - o : pkv::kHostChunkBytes;
+      const size_t k = next++ % n_copy;
+      if (hipMemcpyAsync(dst + c.off + o, src + c.off + o, n, hipMemcpyHostToDevice,
+                         static_cast<hipStream_t>(p->copy_streams[k])) != hipSuccess)
+        return false;
+      used |= 1u << k;
+    }
+    return true;
+  };
   for (int64_t l = 0; l < L; ++l) {
-    for (int64_t i = h.payload_layer[l]; i < h.payload_layer[l + 1]; ++i) {
-      const pkv::CopyRange& c = h.payload_ranges[size_t(i)];
-      if (hipMemcpyAsync(dp_bytes + c.off, hp_bytes + c.off, c.len, hipMemcpyHostToDevice, copy_stream(l)) !=
-          hipSuccess)
+    uint32_t used = 0;
+    for (int64_t i = h.payload_layer[l]; i < h.payload_layer[l + 1]; ++i)
+      if (!enqueue(dp_bytes, hp_bytes, h.payload_ranges[size_t(i)], used)) return PKV_ERR_DEVICE;
+    for (int64_t i = h.scale_layer[l]; i < h.scale_layer[l + 1]; ++i)
+      if (!enqueue(ds_bytes, hs_bytes, h.scale_ranges[size_t(i)], used)) return PKV_ERR_DEVICE;
+    for (size_t k = 0; k < n_copy; ++k) {
+      if (!(used & (1u << k))) continue;
+      hipEvent_t e = ev(1 + l * int64_t(n_copy) + int64_t(k));
+      if (hipEventRecord(e, static_cast<hipStream_t>(p->copy_streams[k])) != hipSuccess ||
+          hipStreamWaitEvent(stream, e, 0) != hipSuccess)
         return PKV_ERR_DEVICE;
     }
-    for (int64_t i = h.scale_layer[l]; i < h.scale_layer[l + 1]; ++i) {
-      const pkv::CopyRange& c = h.scale_ranges[size_t(i)];
-      if (hipMemcpyAsync(ds_bytes + c.off, hs_bytes + c.off, c.len, hipMemcpyHostToDevice, copy_stream(l)) !=
-          hipSuccess)
-        return PKV_ERR_DEVICE;
-    }
-    if (hipEventRecord(ev(1 + l), copy_stream(l)) != hipSuccess ||
-        hipStreamWaitEvent(stream, ev(1 + l), 0) != hipSuccess)
-      return PKV_ERR_DEVICE;
     const int64_t u0 = h.layer_units[l], n = h.layer_units[l + 1] - u0;
     if (n == 0) continue;
     st = pkv::launch_restore(plan, payload, scales, k_cache, v_cache, u0, n, stream);

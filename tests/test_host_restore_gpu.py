@@ -132,3 +132,45 @@ def test_streamed_argument_errors(torch):
     assert pb.load().pkv_restore_from_host(ck.handle, *good) == pb.PKV_ERR_INVALID_ARGUMENT
     torch.cuda.synchronize()
     check_full(dr, ckpt)  # nothing above wrote anything
+
+
+def test_zero_copy_restore_from_pinned_memory(torch):
+    """pkv_restore reading the checkpoint straight from pinned host memory:
+    the same caches as the oracle and as a device-resident restore."""
+    case = wl.make_custom(12, L=3, H=4, D=128, B=32, P=16, n_tokens=(300, 95), deltas=(-700, 3), rho0s=(900, 4),
+                          tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2, out_dtype=wl.OUT_BF16,
+                          outlier_pairs=1)
+    dr, ckpt = _streamed(case, torch)  # device-resident reference via the streamed path
+    k_ref, v_ref = dr.host_caches()
+    hp = torch.from_numpy(ckpt[0]).pin_memory()
+    hs = torch.from_numpy(ckpt[1].view(np.int16)).pin_memory()
+    dr.prefill()
+    pb.restore_tensors(dr.plan, hp, hs, dr.k_cache, dr.v_cache)
+    torch.cuda.synchronize()
+    k, v = dr.host_caches()
+    assert np.array_equal(k, k_ref) and np.array_equal(v, v_ref)
+    check_full(dr, ckpt)
+
+
+def test_pageable_and_foreign_inputs_rejected(torch):
+    """Inputs the kernel could not read are refused before any launch."""
+    case = wl.make_case("tiny")
+    dr, ckpt = _streamed(case, torch)
+    before = dr.host_caches()
+    nb = lambda t: t.numel() * t.element_size()
+    pageable_p = np.ascontiguousarray(ckpt[0])
+    pageable_s = np.ascontiguousarray(ckpt[1])
+    args = (pageable_p.ctypes.data, pageable_p.nbytes, dr.scales.data_ptr(), nb(dr.scales), dr.k_cache.data_ptr(),
+            dr.v_cache.data_ptr(), nb(dr.k_cache), 0)
+    assert pb.pkv_restore_status(dr.plan, *args) == pb.PKV_ERR_INVALID_ARGUMENT
+    args = (dr.payload.data_ptr(), nb(dr.payload), pageable_s.ctypes.data, pageable_s.nbytes, dr.k_cache.data_ptr(),
+            dr.v_cache.data_ptr(), nb(dr.k_cache), 0)
+    assert pb.pkv_restore_status(dr.plan, *args) == pb.PKV_ERR_INVALID_ARGUMENT
+    # caches must be device memory
+    hk = torch.empty(dr.k_cache.numel(), dtype=torch.int16, pin_memory=True)
+    args = (dr.payload.data_ptr(), nb(dr.payload), dr.scales.data_ptr(), nb(dr.scales), hk.data_ptr(),
+            dr.v_cache.data_ptr(), nb(dr.k_cache), 0)
+    assert pb.pkv_restore_status(dr.plan, *args) == pb.PKV_ERR_INVALID_ARGUMENT
+    torch.cuda.synchronize()
+    after = dr.host_caches()
+    assert np.array_equal(before[0], after[0]) and np.array_equal(before[1], after[1])

@@ -260,6 +260,26 @@ pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, co
                                  uint64_t cache_bytes, void* payload, uint64_t payload_bytes, void* scales,
                                  uint64_t scale_bytes, void* hip_stream);
 
+/* ----------------------------------------------------------------------------
+ * Resume planner (Section IV-B, Eq. 9, 11, 12): the block-aligned repair set
+ * R of one request, as the repair_mask a pkv_request_t takes.  Host only.
+ *   D = { i in S : i < min(dirty_tokens, N) }        (Eq. 9; token i of S is
+ *       i tokens past the edit, and dirty_tokens is the length model's
+ *       prediction d_hat, computed elsewhere);
+ *   H = the k highest importance[i] over i in S \ D  (Eq. 11), with
+ *       k = floor(kappa * |S \ D| + 1/2) in double precision and ties
+ *       broken toward the smaller i;
+ *   R = the blocks of B tokens that meet D u H, F = the rest (Eq. 12).
+ *   suffix_tokens  : N >= 0;  block_tokens : B, 1 <= B <= 1024;
+ *   dirty_tokens   : d_hat >= 0 (values past N mean all of S);
+ *   importance     : host [N] stored scores I_i(0), finite (may be NULL when N == 0);
+ *   kappa          : the nonlocal budget fraction, 0 <= kappa <= 1;
+ *   repair_mask    : host [ceil(N / B)] output, 1 = block in R, 0 = in F;
+ *   nonlocal_tokens: output |H| (may be NULL).
+ * Errors: PKV_ERR_INVALID_ARGUMENT, PKV_ERR_OUT_OF_MEMORY. */
+pkv_status_t pkv_plan_repair(int32_t suffix_tokens, int32_t block_tokens, int64_t dirty_tokens,
+                             const float* importance, double kappa, uint8_t* repair_mask, int64_t* nonlocal_tokens);
+
 /* What a plan reads and writes (for sizing buffers and for bandwidth
  * accounting).  For a checkpoint plan, bytes_read counts cache rows read and
  * bytes_written the payload and scale bytes written; restored_rows counts the

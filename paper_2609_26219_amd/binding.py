@@ -25,7 +25,7 @@ PKV_ERR_DEVICE = -7
 
 # Every symbol include/pkv.h declares.
 EXPORTED = ("pkv_payload_size", "pkv_restore_plan", "pkv_restore", "pkv_restore_from_host", "pkv_free",
-            "pkv_plan_query", "pkv_status_string", "pkv_checkpoint_plan", "pkv_quantize_gather")
+            "pkv_plan_query", "pkv_status_string", "pkv_checkpoint_plan", "pkv_quantize_gather", "pkv_plan_repair")
 
 
 class PkvModel(ctypes.Structure):
@@ -94,6 +94,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pkv_checkpoint_plan.restype = i32
     lib.pkv_quantize_gather.argtypes = [vp, vp, vp, u64, vp, u64, vp, u64, vp]
     lib.pkv_quantize_gather.restype = i32
+    lib.pkv_plan_repair.argtypes = [i32, i32, ctypes.c_int64, vp, ctypes.c_double, vp, ctypes.POINTER(ctypes.c_int64)]
+    lib.pkv_plan_repair.restype = i32
     _lib = lib
     return lib
 
@@ -195,6 +197,26 @@ def quantize_gather_tensors(plan: "Plan", k_cache, v_cache, payload, scales, str
     nbytes = lambda t: t.numel() * t.element_size()
     pkv_quantize_gather(plan, k_cache.data_ptr(), v_cache.data_ptr(), nbytes(k_cache), payload.data_ptr(),
                         nbytes(payload), scales.data_ptr(), nbytes(scales), stream.cuda_stream)
+
+
+def pkv_plan_repair(suffix_tokens: int, block_tokens: int, dirty_tokens: int, importance, kappa: float):
+    """Resume planner: (repair mask uint8 [ceil(N/B)], |H|)."""
+    imp = np.ascontiguousarray(importance, dtype=np.float32)
+    assert imp.size == suffix_tokens
+    nb = -(-int(suffix_tokens) // int(block_tokens)) if block_tokens > 0 else 0
+    mask = np.zeros(max(1, nb), np.uint8)
+    h = ctypes.c_int64()
+    st = load().pkv_plan_repair(int(suffix_tokens), int(block_tokens), int(dirty_tokens),
+                                imp.ctypes.data if imp.size else None, float(kappa), mask.ctypes.data,
+                                ctypes.byref(h))
+    if st != PKV_OK:
+        raise PkvError(st, "pkv_plan_repair")
+    return mask[:nb], int(h.value)
+
+
+def pkv_plan_repair_status(suffix_tokens, block_tokens, dirty_tokens, importance_ptr, kappa, mask_ptr) -> int:
+    return load().pkv_plan_repair(int(suffix_tokens), int(block_tokens), int(dirty_tokens), importance_ptr,
+                                  float(kappa), mask_ptr, None)
 
 
 def pkv_payload_size(shape, request):

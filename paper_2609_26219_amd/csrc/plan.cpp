@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <limits>
 #include <new>
 #include <tuple>
@@ -426,6 +427,41 @@ pkv_status_t pkv_internal_host_units(const pkv_model_t* model, const pkv_request
   *count = int64_t(hp.units.size());
   if (units_out && capacity >= *count && *count > 0)
     memcpy(units_out, hp.units.data(), hp.units.size() * sizeof(pkv::Unit));
+  return PKV_OK;
+}
+
+pkv_status_t pkv_plan_repair(int32_t suffix_tokens, int32_t block_tokens, int64_t dirty_tokens,
+                             const float* importance, double kappa, uint8_t* repair_mask, int64_t* nonlocal_tokens) {
+  if (suffix_tokens < 0 || block_tokens < 1 || block_tokens > pkv::kMaxBlockTokens || dirty_tokens < 0)
+    return PKV_ERR_INVALID_ARGUMENT;
+  if (!(kappa >= 0.0 && kappa <= 1.0)) return PKV_ERR_INVALID_ARGUMENT;
+  const int64_t N = suffix_tokens, B = block_tokens, nb = (N + B - 1) / B;
+  if (N > 0 && (!importance || !repair_mask)) return PKV_ERR_INVALID_ARGUMENT;
+  for (int64_t i = 0; i < N; ++i)
+    if (!std::isfinite(importance[i])) return PKV_ERR_INVALID_ARGUMENT;
+  const int64_t d = std::min<int64_t>(dirty_tokens, N);
+  const int64_t candidates = N - d;
+  int64_t k = int64_t(std::floor(kappa * double(candidates) + 0.5));
+  k = std::min<int64_t>(std::max<int64_t>(k, 0), candidates);
+  try {
+    std::vector<uint8_t> mask(size_t(nb), 0);
+    // Eq. 9: the dirty window D = [0, d) rounds to blocks [0, ceil(d / B)).
+    for (int64_t b = 0; b < (d + B - 1) / B; ++b) mask[size_t(b)] = 1;
+    // Eq. 11: the k best-scoring candidates (score descending, index ascending).
+    if (k > 0) {
+      std::vector<std::pair<float, int32_t>> cand(static_cast<size_t>(candidates));
+      for (int64_t i = 0; i < candidates; ++i) cand[size_t(i)] = {importance[d + i], int32_t(d + i)};
+      auto better = [](const std::pair<float, int32_t>& a, const std::pair<float, int32_t>& b) {
+        return a.first > b.first || (a.first == b.first && a.second < b.second);
+      };
+      if (k < candidates) std::nth_element(cand.begin(), cand.begin() + (k - 1), cand.end(), better);
+      for (int64_t j = 0; j < k; ++j) mask[size_t(cand[size_t(j)].second / B)] = 1;  // Eq. 12
+    }
+    std::copy(mask.begin(), mask.end(), repair_mask);
+  } catch (const std::bad_alloc&) {
+    return PKV_ERR_OUT_OF_MEMORY;
+  }
+  if (nonlocal_tokens) *nonlocal_tokens = k;
   return PKV_OK;
 }
 

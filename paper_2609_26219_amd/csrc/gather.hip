@@ -25,12 +25,14 @@
 // largest binary16 not above the minimum, the scale the smallest binary16
 // not below (max - zero)/(2^bits - 1) (both in double), and a code is
 // round-half-even((x - zero)/scale) with the quotient correctly rounded in
-// double.  Codes are first formed in float as floor((x - zero) * (1/scale) +
-// 1/2); that float value is within 5e-5 of the exact quotient + 1/2 (three
-// roundings of 2^-24 relative on a quotient <= 255, plus the final one), so
-// whenever it lies farther than 1e-4 from an integer its floor is the exact
-// rounding; a packed word of codes (8 four-bit or 4 eight-bit) with any value
-// closer is recomputed in double with a true division.
+// double.  Codes are first formed in float: t = (x - zero) * (1/scale), which
+// is within 5e-5 of the exact quotient (three roundings of 2^-24 relative on
+// a quotient <= 255), rounded to the nearest integer by the hardware's float
+// to byte conversion.  Whenever t lies farther than 1e-4 from a half-integer
+// that is the exact rounding, and it never exceeds 2^bits - 1 (the scale is
+// rounded up), so no clip is needed; a packed word of codes (8 four-bit or 4
+// eight-bit) with any t closer to a half-integer is recomputed in double with
+// a true division.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -104,29 +106,33 @@ struct Quant {
   double zero, scale;
 };
 
-// Codes of the first N values of w (x >= zero, scale > 0) packed into one
-// word: N = 8 four-bit codes (nibble e) or N = 4 eight-bit codes (byte e).
-// v = (x - zero) * (1/scale) + 1/2 is formed in float (fma, one rounding) and
-// the code is floor(v), clipped.  `near` is set when some v lies within 1e-4
-// of an integer, where the float quotient cannot decide the rounding; the
-// caller then uses encode_exact.
+// Codes of the first N values of w (zero <= x <= max of the tile) packed into
+// one word: N = 8 four-bit codes (nibble e) or N = 4 eight-bit codes (byte e).
+// t = (x - zero) * (1/scale) is formed in float and v_cvt_pk_u8_f32 rounds it
+// to nearest even into a byte (it saturates to [0, 255]; t never leaves
+// [0, 2^bits - 1] by more than 5e-5, so no code needs a clip).  Four-bit codes
+// of even and odd channels go to the bytes of two words that are then merged
+// nibble-wise.  `near` is set when some t lies within 1e-4 of a half-integer,
+// where the float quotient cannot decide the rounding; the caller then uses
+// encode_exact.  With scale 0 (invf = 0) every t is 0.
+constexpr float kTieWindow = 1e-4f;
+
 template <bool BF16, int N>
 __device__ __forceinline__ uint32_t encode_fast(const uint4& w, const Quant& q, bool& near) {
-  constexpr int kBits = 32 / N;
-  uint32_t packed = 0;
-  bool tie = false;
+  uint32_t lo = 0, hi = 0;  // N == 4: the codes; N == 8: even / odd channels, one per byte
+  float dist = 1.0f;        // min over values of |frac(t) - 1/2|
 #pragma unroll
   for (int e = 0; e < N; ++e) {
     const float x = cache_value<BF16>(word_of(w, e), e & 1);
-    const float v = __builtin_fmaf(x - q.zf, q.invf, 0.5f);
-    uint32_t k = static_cast<uint32_t>(v);  // v > 0: truncation is floor
-    k = k < q.qmax ? k : q.qmax;
-    const float f = __builtin_amdgcn_fractf(v);
-    tie |= __builtin_fabsf(f - 0.5f) > 0.4999f;
-    packed |= k << (kBits * e);
+    const float t = (x - q.zf) * q.invf;
+    if (N == 4 || !(e & 1))
+      lo = __builtin_amdgcn_cvt_pk_u8_f32(t, N == 4 ? e : e >> 1, lo);
+    else
+      hi = __builtin_amdgcn_cvt_pk_u8_f32(t, e >> 1, hi);
+    dist = __builtin_fminf(dist, __builtin_fabsf(__builtin_amdgcn_fractf(t) - 0.5f));
   }
-  near = tie;
-  return packed;
+  near = dist < kTieWindow;
+  return N == 4 ? lo : lo | (hi << 4);
 }
 
 // The same codes from the definition in double: rint((x - zero) / scale)
@@ -345,7 +351,7 @@ struct TileHdr {
   uint32_t tile_bytes;  // B * H * D * bits / 8
   uint32_t* scale_word;
   int64_t row0;
-  int32_t n_valid, bits, head, first_page;
+  int32_t n_valid, bits, head;
   int32_t page0, page1, page2;  // kUnitPages source pages
 };
 
@@ -367,7 +373,6 @@ __device__ __forceinline__ TileHdr tile_header(const GatherArgs& a, const Unit* 
   h.bits = which ? kValueBits[tag] : kKeyBits[tag];
   h.tile_bytes = uint32_t(a.B) * uint32_t(a.H) * uint32_t(a.D) * uint32_t(h.bits) / 8u;
   h.head = head;
-  h.first_page = int32_t(u.row0 >> a.log2P);
   h.page0 = __builtin_amdgcn_readfirstlane(u.page0);
   h.page1 = __builtin_amdgcn_readfirstlane(u.page1);
   h.page2 = __builtin_amdgcn_readfirstlane(u.page2);
@@ -385,13 +390,15 @@ __device__ __forceinline__ void load_tile(const GatherArgs& a, const TileHdr& h,
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(h.src), 0, h.range, 0x00020000);
   const uint32_t row_bytes = uint32_t(a.H) * uint32_t(a.D) * 2u;
   const uint32_t slot_mask = (1u << a.log2P) - 1;
+  const uint32_t slot0 = uint32_t(h.row0) & slot_mask;  // the block's first row within its first page
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
     const int t = i * a.rpl + r;
-    const int64_t row = h.row0 + (t < h.n_valid ? t : 0);
-    const int k = int32_t(row >> a.log2P) - h.first_page;  // 0, 1 or 2
-    const uint32_t page = uint32_t(h.page0 + (k >= 1 ? h.page1 - h.page0 : 0) + (k >= 2 ? h.page2 - h.page1 : 0));
-    const uint32_t off = ((page << a.log2P) | (uint32_t(row) & slot_mask)) * row_bytes + 16u * uint32_t(c);
+    const uint32_t pos = slot0 + uint32_t(t < h.n_valid ? t : 0);  // rows from the first page's start
+    const uint32_t k = pos >> a.log2P;                               // 0, 1 or 2
+    const uint32_t page = uint32_t(h.page0) + (k >= 1 ? uint32_t(h.page1 - h.page0) : 0u) +
+                          (k >= 2 ? uint32_t(h.page2 - h.page1) : 0u);
+    const uint32_t off = ((page << a.log2P) | (pos & slot_mask)) * row_bytes + 16u * uint32_t(c);
     w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0));
   }
 }
@@ -414,7 +421,7 @@ __device__ __forceinline__ uint4 fresh(uint4 w) {
 // encodes and writes; every store is issued (a lane with nothing to write
 // gets an offset past the tile's buffer range, which the hardware drops).
 template <bool BF16, int NL>
-__device__ __forceinline__ Quant tile_range(const GatherArgs& a, const TileHdr& h, int r, bool on, uint4 (&w)[NL],
+__device__ __forceinline__ Quant tile_range(const GatherArgs& a, const TileHdr& h, int r, uint4 (&w)[NL],
                                             uint16_t& sb, uint16_t& zb) {
   Quant q;
   if (h.bits == 16) {
@@ -426,22 +433,28 @@ __device__ __forceinline__ Quant tile_range(const GatherArgs& a, const TileHdr& 
     sb = zb = 0;
     return q;
   }
+  // Every loaded value belongs to the tile (rows past n_valid and idle lanes
+  // load rows of the block), so the range runs over all of them unmasked.
+  // For bf16 the high value of a word is compared as the raw 32-bit word:
+  // its low half only adds less than one bf16 step of magnitude, which never
+  // changes the order against another value, and is cleared at the end.
   float mn = __builtin_inff(), mx = -__builtin_inff();
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
-    const int t = i * a.rpl + r;
-    float pmn = __builtin_inff(), pmx = -__builtin_inff();
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float x = cache_value<BF16>(word_of(w[i], e), e & 1);
-      pmn = __builtin_fminf(pmn, x);
-      pmx = __builtin_fmaxf(pmx, x);
+    for (int p = 0; p < 4; ++p) {
+      const uint32_t word = word_of(w[i], 2 * p);
+      const float x0 = cache_value<BF16>(word, 0);
+      const float x1 = BF16 ? __uint_as_float(word) : cache_value<BF16>(word, 1);
+      mn = __builtin_fminf(__builtin_fminf(mn, x0), x1);
+      mx = __builtin_fmaxf(__builtin_fmaxf(mx, x0), x1);
     }
-    const bool ok = on && t < h.n_valid;
-    mn = ok ? __builtin_fminf(mn, pmn) : mn;
-    mx = ok ? __builtin_fmaxf(mx, pmx) : mx;
   }
   wave_range(mn, mx);
+  if (BF16) {
+    mn = __uint_as_float(__float_as_uint(mn) & 0xFFFF0000u);
+    mx = __uint_as_float(__float_as_uint(mx) & 0xFFFF0000u);
+  }
   const double qmax = double((1 << h.bits) - 1);
   zb = f16_floor(static_cast<double>(mn) + 0.0);  // -0 counts as +0
   q.zero = f16_value(zb);
@@ -506,7 +519,7 @@ __global__ __launch_bounds__(kGatherMaxWaves * 64) void gather_tile_kernel(TileA
   uint4 w[NL];
   uint16_t sb, zb;
   load_tile<NL>(a, h, r, c, w);
-  const Quant q = tile_range<BF16, NL>(a, h, r, on, w, sb, zb);
+  const Quant q = tile_range<BF16, NL>(a, h, r, w, sb, zb);
   tile_store<BF16, NL>(a, h, r, c, on, w, q, sb, zb);
 }
 

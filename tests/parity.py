@@ -302,3 +302,51 @@ def reused_byte_masks(case, gap: int = 0):
                 so = case.layer_scale_offset(ri, layer)
                 smask[so: so + nb * H * 4] = True
     return pmask, smask
+
+
+# ---------------------------------------------------------------------------
+# Checkpoint write
+# ---------------------------------------------------------------------------
+
+FILL = 0xAB  # checkpoint-write tests: payload bytes outside every checkpoint range keep this
+
+
+def gpu_checkpoint(case, torch, caches=None):
+    """Write a case's checkpoint on the GPU from its old caches (host arrays
+    unless given); payload and scales start filled with marker values."""
+    from paper_2609_26219_amd import binding as pb
+
+    s = case.src_shape
+    kc, vc = case.host_old_caches() if caches is None else caches
+    dk = torch.from_numpy(kc.view(np.int16)).cuda()
+    dv = torch.from_numpy(vc.view(np.int16)).cuda()
+    payload = torch.full((case.payload_nbytes,), FILL, dtype=torch.uint8, device="cuda")
+    scales = torch.full((case.scale_elems,), 0x5A5A, dtype=torch.int16, device="cuda")
+    plan = pb.pkv_checkpoint_plan(s, case.requests)
+    info = pb.pkv_plan_query(plan)
+    assert info["kind"] == 1
+    pb.quantize_gather_tensors(plan, dk, dv, payload, scales)
+    torch.cuda.synchronize()
+    return kc, vc, payload.cpu().numpy(), scales.cpu().numpy().view(np.uint16), info
+
+
+def check_checkpoint_write(case, torch, caches=None):
+    """The GPU checkpoint write against the oracle quantizer, bit for bit;
+    bytes outside every request's ranges keep their marker values."""
+    from oracle import quantize as oq
+    from paper_2609_26219_amd import workloads as wl
+
+    kc, vc, payload, scales, info = gpu_checkpoint(case, torch, caches)
+    ref_p, ref_s = oq.quantize_gather(case.src_shape, case.requests, kc, vc, case.payload_nbytes, case.scale_elems)
+    inside_p = np.zeros(case.payload_nbytes, bool)
+    inside_s = np.zeros(case.scale_elems, bool)
+    for r in case.requests:
+        pbytes, selems = wl.encoded_request_nbytes(case.shape, r)
+        inside_p[r.payload_offset: r.payload_offset + pbytes] = True
+        inside_s[r.scale_offset: r.scale_offset + selems] = True
+    bad = np.nonzero(payload[inside_p] != ref_p[inside_p])[0]
+    assert bad.size == 0, f"{bad.size} payload bytes differ, first at {bad[:5]}"
+    assert np.array_equal(scales[inside_s], ref_s[inside_s])
+    assert (payload[~inside_p] == FILL).all() and (scales[~inside_s] == 0x5A5A).all()
+    assert info["bytes_written"] == int(inside_p.sum()) + 2 * int(inside_s.sum())
+    return payload, scales, ref_p, ref_s

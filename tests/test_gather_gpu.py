@@ -4,15 +4,12 @@ import numpy as np
 import pytest
 
 import oracle
-from oracle import quantize as oq
 from paper_2609_26219_amd import binding as pb
 from paper_2609_26219_amd import workloads as wl
 
-from parity import Stats, log
+from parity import Stats, check_checkpoint_write, log
 
 pytestmark = pytest.mark.gpu
-
-FILL = 0xAB  # payload bytes outside every checkpoint range must keep this
 
 
 @pytest.fixture(scope="module")
@@ -24,42 +21,10 @@ def torch():
     return _t
 
 
-def _gpu_checkpoint(case, torch, caches=None):
-    s = case.src_shape
-    kc, vc = case.host_old_caches() if caches is None else caches
-    dk = torch.from_numpy(kc.view(np.int16)).cuda()
-    dv = torch.from_numpy(vc.view(np.int16)).cuda()
-    payload = torch.full((case.payload_nbytes,), FILL, dtype=torch.uint8, device="cuda")
-    scales = torch.full((case.scale_elems,), 0x5A5A, dtype=torch.int16, device="cuda")
-    plan = pb.pkv_checkpoint_plan(s, case.requests)
-    info = pb.pkv_plan_query(plan)
-    assert info["kind"] == 1
-    pb.quantize_gather_tensors(plan, dk, dv, payload, scales)
-    torch.cuda.synchronize()
-    return kc, vc, payload.cpu().numpy(), scales.cpu().numpy().view(np.uint16), info
-
-
-def _check_against_oracle(case, torch, caches=None):
-    kc, vc, payload, scales, info = _gpu_checkpoint(case, torch, caches)
-    ref_p, ref_s = oq.quantize_gather(case.src_shape, case.requests, kc, vc, case.payload_nbytes, case.scale_elems)
-    inside_p = np.zeros(case.payload_nbytes, bool)
-    inside_s = np.zeros(case.scale_elems, bool)
-    for r in case.requests:
-        pbytes, selems = wl.encoded_request_nbytes(case.shape, r)
-        inside_p[r.payload_offset: r.payload_offset + pbytes] = True
-        inside_s[r.scale_offset: r.scale_offset + selems] = True
-    bad = np.nonzero(payload[inside_p] != ref_p[inside_p])[0]
-    assert bad.size == 0, f"{bad.size} payload bytes differ, first at {bad[:5]}"
-    assert np.array_equal(scales[inside_s], ref_s[inside_s])
-    assert (payload[~inside_p] == FILL).all() and (scales[~inside_s] == 0x5A5A).all()
-    assert info["bytes_written"] == int(inside_p.sum()) + 2 * int(inside_s.sum())
-    return payload, scales, ref_p, ref_s
-
-
 @pytest.mark.parametrize("name,int4", [("tiny", wl.TAG_K8V4), ("tiny", wl.TAG_K4V4), ("llama8b_1l", wl.TAG_K8V4)])
 def test_checkpoint_bit_exact_named(name, int4, torch):
     log(f"[gpu] checkpoint write {name}")
-    _check_against_oracle(wl.make_case(name, int4_tag=int4), torch)
+    check_checkpoint_write(wl.make_case(name, int4_tag=int4), torch)
 
 
 @pytest.mark.parametrize("params", [
@@ -77,7 +42,7 @@ def test_checkpoint_bit_exact_named(name, int4, torch):
         "h20_d16", "d48_idle_lanes", "general_nl4", "general_nl2"])
 def test_checkpoint_bit_exact_custom(params, torch):
     case = wl.make_custom(11, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), outlier_pairs=1, **params)
-    _check_against_oracle(case, torch)
+    check_checkpoint_write(case, torch)
 
 
 @pytest.mark.parametrize("out", [wl.OUT_FP16, wl.OUT_BF16])
@@ -102,7 +67,7 @@ def test_checkpoint_exact_and_near_ties(out, torch):
                 bits[:, :, 0] = wl.to_cache_bits(np.zeros(1), out)[0]   # min 0: zero 0
                 bits[:, :, 1] = wl.to_cache_bits(np.full(1, 15 * step), out)[0]  # max 15 * step
                 flat[slots] = bits.astype(np.uint16)
-    _check_against_oracle(case, torch, (kc, vc))
+    check_checkpoint_write(case, torch, (kc, vc))
 
 
 def test_write_then_restore_cycle(torch):
@@ -110,7 +75,7 @@ def test_write_then_restore_cycle(torch):
     with the key phase shift, compared element by element with the oracle's
     restore of the oracle's own checkpoint."""
     case = wl.make_case("llama8b_1l")
-    payload, scales, ref_p, ref_s = _check_against_oracle(case, torch)
+    payload, scales, ref_p, ref_s = check_checkpoint_write(case, torch)
     s = case.shape
     dpay = torch.from_numpy(payload).cuda()
     dsc = torch.from_numpy(scales.view(np.int16)).cuda()

@@ -1,0 +1,17 @@
+"""CPU side of the parity sweep: every seeded random configuration is a valid
+model and resume (the host planner accepts it), and the address replays of
+both kernels (restore and checkpoint write) stay in bounds and cover exactly
+the rows they must."""
+import pytest
+
+from sweep import SWEEP_SIZE, describe, sweep_case
+from test_gather_indexing import emulate as emulate_checkpoint_write
+from test_kernel_indexing import emulate as emulate_restore
+
+
+@pytest.mark.parametrize("i", range(SWEEP_SIZE))
+def test_sweep_addresses(i):
+    case = sweep_case(i)
+    print(describe(case))
+    emulate_restore(case)
+    emulate_checkpoint_write(case)

@@ -1,0 +1,28 @@
+"""GPU side of the parity sweep: for every seeded random configuration, the
+restore against a full oracle restore (every cache byte) and the checkpoint
+write against the oracle quantizer (bit for bit)."""
+import pytest
+
+from paper_2609_26219_amd import binding as pb
+from parity import check_checkpoint_write, check_full, log, restore_small
+from sweep import SWEEP_SIZE, describe, sweep_case
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _t
+    if not _t.cuda.is_available():
+        pytest.skip("no GPU")
+    pb.load()
+    return _t
+
+
+@pytest.mark.parametrize("i", range(SWEEP_SIZE))
+def test_sweep_parity(i, torch):
+    case = sweep_case(i)
+    log(f"[gpu] sweep {i}: {describe(case)}")
+    st = check_full(*restore_small(case))
+    log(f"  restore {st}")
+    check_checkpoint_write(case, torch)

@@ -363,7 +363,7 @@ def main():
                     help="representation of the int4 tag: K8V4 (the paper's tier) or uniform K4V4")
     ap.add_argument("--sets", type=int, default=2, help="buffer sets cycled between steps")
     ap.add_argument("--write-steps", type=int, default=10, help="timed checkpoint-write launches")
-    ap.add_argument("--host-steps", type=int, default=5, help="timed streamed restores from pinned host memory")
+    ap.add_argument("--host-steps", type=int, default=10, help="timed streamed restores from pinned host memory")
     ap.add_argument("--no-representations", action="store_true",
                     help="skip the uniform-representation comparison (FP16 / K8V8 / K8V4 / K4V4 / mixed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

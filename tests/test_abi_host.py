@@ -294,3 +294,15 @@ def test_checkpoint_plan_any_valid_model(H, D, B):
 def test_plan_kinds_are_not_interchangeable(lib):
     # without a GPU no plan can be built; the kind check itself is exercised on the GPU
     assert lib.pkv_quantize_gather(None, None, None, 0, None, 0, None, 0, None) == pb.PKV_ERR_INVALID_ARGUMENT
+
+
+def test_missing_library_fails_loudly():
+    """No fallback: without libpkv.so the binding raises instead of running
+    anything else."""
+    saved = pb._lib
+    pb._lib = None
+    try:
+        with pytest.raises(ImportError):
+            pb.load("/nonexistent/libpkv.so")
+    finally:
+        pb._lib = saved

@@ -52,3 +52,19 @@ def describe(case) -> str:
             f"R={s.rotary_dim or s.head_dim} scaled={s.inv_freq is not None} theta={s.rope_theta:g} "
             f"reqs={[(q.suffix_tokens, q.delta, q.dst_row0) for q in case.requests]} "
             f"tags={sorted(set(int(t) for q in case.requests for t in q.tags))}")
+
+
+# Configurations at the limits the planner accepts: rows of H * D = 4096
+# elements (the largest), head_dim 512 (the largest), blocks of 1024 tokens
+# (the largest), one-token and 1024-token pages.
+LIMIT_CASES = {
+    "hd4096_h32_d128": dict(L=1, H=32, D=128, B=8, P=8, n_tokens=(61, 17), deltas=(-300, 7), rho0s=(5, 3)),
+    "hd4096_h8_d512": dict(L=2, H=8, D=512, B=4, P=2, n_tokens=(23,), deltas=(9000,), rho0s=(1,)),
+    "b1024_p1024": dict(L=1, H=2, D=64, B=1024, P=1024, n_tokens=(2500,), deltas=(-5,), rho0s=(1000,)),
+    "b1024_p1": dict(L=1, H=1, D=32, B=1024, P=1, n_tokens=(1100,), deltas=(3,), rho0s=(2,)),
+}
+
+
+def limit_case(name: str) -> "wl.Case":
+    return wl.make_custom(77, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2, out_dtype=wl.OUT_BF16,
+                          outlier_pairs=1, **LIMIT_CASES[name])

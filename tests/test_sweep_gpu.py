@@ -5,7 +5,7 @@ import pytest
 
 from paper_2609_26219_amd import binding as pb
 from parity import check_checkpoint_write, check_full, log, restore_small
-from sweep import SWEEP_SIZE, describe, sweep_case
+from sweep import LIMIT_CASES, SWEEP_SIZE, describe, limit_case, sweep_case
 
 pytestmark = pytest.mark.gpu
 
@@ -23,6 +23,15 @@ def torch():
 def test_sweep_parity(i, torch):
     case = sweep_case(i)
     log(f"[gpu] sweep {i}: {describe(case)}")
+    st = check_full(*restore_small(case))
+    log(f"  restore {st}")
+    check_checkpoint_write(case, torch)
+
+
+@pytest.mark.parametrize("name", sorted(LIMIT_CASES))
+def test_limit_parity(name, torch):
+    case = limit_case(name)
+    log(f"[gpu] limits {name}: {describe(case)}")
     st = check_full(*restore_small(case))
     log(f"  restore {st}")
     check_checkpoint_write(case, torch)

@@ -196,9 +196,12 @@ pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t p
  *   k_cache, v_cache, cache_bytes, hip_stream : as in pkv_restore.
  * Returns after enqueueing; everything is complete once `hip_stream` has
  * passed the last layer.  The host buffers must stay valid until then.
- * Calls on one plan must not overlap (they share its copy streams), and the
- * plan must be a restore plan.  The streams and events are created on
- * the first call and released by pkv_free.  Errors: PKV_ERR_INVALID_ARGUMENT,
+ * Calls on one plan share its copy streams and events, so they must not
+ * overlap: not from two host threads at once, and a call on another stream
+ * must wait until the earlier call's work has finished (successive calls on
+ * one stream are ordered by it).  The plan must be a restore plan.  The
+ * streams and events are created on the first call and released by
+ * pkv_free.  Errors: PKV_ERR_INVALID_ARGUMENT,
  * PKV_ERR_DEVICE. */
 pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payload, uint64_t host_payload_bytes,
                                    const void* host_scales, uint64_t host_scale_bytes, void* payload,

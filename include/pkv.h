@@ -170,7 +170,9 @@ pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* req
  * until the stream has passed the restore.  Calls that share a plan are safe
  * concurrently only on disjoint caches.  Errors: PKV_ERR_INVALID_ARGUMENT,
  * PKV_ERR_DEVICE (launch failure; asynchronous faults surface at the next
- * synchronisation of the stream). */
+ * synchronisation of the stream).  The call enqueues one kernel and allocates
+ * nothing, so it may be captured in a HIP graph; the checks above then run
+ * once, at capture, and every replay uses the captured pointers. */
 pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t payload_bytes, const void* scales,
                          uint64_t scale_bytes, void* k_cache, void* v_cache, uint64_t cache_bytes, void* hip_stream);
 
@@ -258,7 +260,9 @@ pkv_status_t pkv_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoint_
  *                       16- / 8-byte aligned, not overlapping each other or the caches.
  * Only bytes inside the requests' checkpoint ranges are written.
  * A restore plan passed here (or a checkpoint plan passed to pkv_restore) is
- * PKV_ERR_INVALID_ARGUMENT.  Errors: PKV_ERR_INVALID_ARGUMENT, PKV_ERR_DEVICE. */
+ * PKV_ERR_INVALID_ARGUMENT.  Errors: PKV_ERR_INVALID_ARGUMENT, PKV_ERR_DEVICE.
+ * Like pkv_restore, it enqueues one kernel, allocates nothing and may be
+ * captured in a HIP graph. */
 pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, const void* v_cache,
                                  uint64_t cache_bytes, void* payload, uint64_t payload_bytes, void* scales,
                                  uint64_t scale_bytes, void* hip_stream);

@@ -32,7 +32,8 @@ class PkvModel(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("block_tokens", ctypes.c_int32), ("page_size", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
                 ("pool_pages", ctypes.c_int64), ("rope_theta", ctypes.c_double), ("rope_style", ctypes.c_int32),
-                ("rotary_dim", ctypes.c_int32), ("inv_freq", ctypes.c_void_p)]
+                ("rotary_dim", ctypes.c_int32), ("inv_freq", ctypes.c_void_p), ("kv_layout", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class PkvRequest(ctypes.Structure):
@@ -113,7 +114,7 @@ def make_model(shape) -> PkvModel:
     m = PkvModel(int(shape.num_layers), int(shape.num_kv_heads), int(shape.head_dim), int(shape.block_tokens),
                  int(shape.page_size), int(shape.out_dtype), int(shape.pool_pages), float(shape.rope_theta),
                  int(getattr(shape, "rope_style", 0)), int(getattr(shape, "rotary_dim", 0)),
-                 freq.ctypes.data if freq is not None and freq.size else None)
+                 freq.ctypes.data if freq is not None and freq.size else None, int(getattr(shape, "kv_layout", 0)), 0)
     m.keep = freq
     return m
 
@@ -188,6 +189,16 @@ def pkv_quantize_gather(plan: "Plan", k_cache: int, v_cache: int, cache_bytes: i
         raise PkvError(st, "pkv_quantize_gather")
 
 
+def cache_nbytes(k_cache, v_cache) -> int:
+    """The cache_bytes argument for torch caches: a tensor's bytes, or, when
+    k_cache and v_cache are the K and V views of one paired cache, the bytes
+    of their shared storage from k_cache on."""
+    ks, vs = k_cache.untyped_storage(), v_cache.untyped_storage()
+    if ks.data_ptr() == vs.data_ptr():
+        return ks.nbytes() - (k_cache.data_ptr() - ks.data_ptr())
+    return k_cache.numel() * k_cache.element_size()
+
+
 def quantize_gather_tensors(plan: "Plan", k_cache, v_cache, payload, scales, stream=None) -> None:
     """Marshal torch device tensors (contiguous) and the current stream into pkv_quantize_gather."""
     import torch
@@ -195,7 +206,7 @@ def quantize_gather_tensors(plan: "Plan", k_cache, v_cache, payload, scales, str
     if stream is None:
         stream = torch.cuda.current_stream(k_cache.device)
     nbytes = lambda t: t.numel() * t.element_size()
-    pkv_quantize_gather(plan, k_cache.data_ptr(), v_cache.data_ptr(), nbytes(k_cache), payload.data_ptr(),
+    pkv_quantize_gather(plan, k_cache.data_ptr(), v_cache.data_ptr(), cache_nbytes(k_cache, v_cache), payload.data_ptr(),
                         nbytes(payload), scales.data_ptr(), nbytes(scales), stream.cuda_stream)
 
 
@@ -311,7 +322,7 @@ def restore_from_host_tensors(plan: Plan, host_payload, host_scales, payload, sc
     nbytes = lambda t: t.numel() * t.element_size()
     pkv_restore_from_host(plan, host_payload.data_ptr(), nbytes(host_payload), host_scales.data_ptr(),
                           nbytes(host_scales), payload.data_ptr(), nbytes(payload), scales.data_ptr(),
-                          nbytes(scales), k_cache.data_ptr(), v_cache.data_ptr(), nbytes(k_cache),
+                          nbytes(scales), k_cache.data_ptr(), v_cache.data_ptr(), cache_nbytes(k_cache, v_cache),
                           stream.cuda_stream)
 
 
@@ -329,4 +340,4 @@ def restore_tensors(plan: Plan, payload, scales, k_cache, v_cache, stream=None) 
         stream = torch.cuda.current_stream(k_cache.device)
     nbytes = lambda t: t.numel() * t.element_size()
     pkv_restore(plan, payload.data_ptr(), nbytes(payload), scales.data_ptr(), nbytes(scales), k_cache.data_ptr(),
-                v_cache.data_ptr(), nbytes(k_cache), stream.cuda_stream)
+                v_cache.data_ptr(), cache_nbytes(k_cache, v_cache), stream.cuda_stream)

@@ -55,8 +55,9 @@ struct GatherArgs {
   const uint16_t* v_cache;
   uint8_t* payload;
   uint16_t* scales;
-  int64_t layer_elems;
+  int64_t layer_elems;  // elements of one layer of a cache (twice pool_pages * P * H * D when paired)
   int32_t H, D, B, log2P;
+  int32_t page_shift;    // slot rows from a layer's start to page p: p << page_shift
   int32_t lpr;     // lanes per row: D / 8
   int32_t rpl;     // rows per load: 64 / lpr
   int32_t nchunk;  // register-resident chunks of NL loads per lane covering the block
@@ -194,7 +195,7 @@ __device__ __forceinline__ void load_chunk(const GatherArgs& a, const TileLane& 
     if (L.on && t < L.n_valid) {
       const int64_t row = L.row0 + t;
       const int64_t page = a.page_tables[L.pt_off + (row >> L.log2P)];
-      w[i] = *reinterpret_cast<const uint4*>(L.src + ((page << L.log2P) | (row & L.slot_mask)) * L.row_elems);
+      w[i] = *reinterpret_cast<const uint4*>(L.src + ((page << a.page_shift) | (row & L.slot_mask)) * L.row_elems);
     }
   }
 }
@@ -398,7 +399,7 @@ __device__ __forceinline__ void load_tile(const GatherArgs& a, const TileHdr& h,
     const uint32_t k = pos >> a.log2P;                               // 0, 1 or 2
     const uint32_t page = uint32_t(h.page0) + (k >= 1 ? uint32_t(h.page1 - h.page0) : 0u) +
                           (k >= 2 ? uint32_t(h.page2 - h.page1) : 0u);
-    const uint32_t off = ((page << a.log2P) | (pos & slot_mask)) * row_bytes + 16u * uint32_t(c);
+    const uint32_t off = ((page << a.page_shift) | (pos & slot_mask)) * row_bytes + 16u * uint32_t(c);
     w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0));
   }
 }
@@ -577,16 +578,19 @@ pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, co
   const pkv_plan_info_t& info = plan->host.info;
   if (info.num_units == 0) return PKV_OK;
   if (!payload || !scales || !k_cache || !v_cache) return PKV_ERR_INVALID_ARGUMENT;
-  if (reinterpret_cast<uintptr_t>(payload) % 16 || reinterpret_cast<uintptr_t>(scales) % 8 ||
-      reinterpret_cast<uintptr_t>(k_cache) % 16 || reinterpret_cast<uintptr_t>(v_cache) % 16)
+  if (reinterpret_cast<uintptr_t>(payload) % 16 || reinterpret_cast<uintptr_t>(scales) % 8)
     return PKV_ERR_INVALID_ARGUMENT;
   if (payload_bytes < info.payload_bytes || scale_bytes < info.scale_bytes || cache_bytes < info.cache_bytes)
     return PKV_ERR_INVALID_ARGUMENT;
-  const uint64_t cb = info.cache_bytes, pb = info.payload_bytes, sb = info.scale_bytes;
-  if (pkv::overlap(payload, pb, scales, sb) || pkv::overlap(payload, pb, k_cache, cb) ||
-      pkv::overlap(payload, pb, v_cache, cb) || pkv::overlap(scales, sb, k_cache, cb) ||
-      pkv::overlap(scales, sb, v_cache, cb))
+  const uint64_t pb = info.payload_bytes, sb = info.scale_bytes;
+  pkv::ByteRange caches[2];
+  int n = 0;
+  if (!pkv::cache_ranges(plan->host.model, k_cache, v_cache, info.cache_bytes, caches, n))
     return PKV_ERR_INVALID_ARGUMENT;
+  if (pkv::overlap(payload, pb, scales, sb)) return PKV_ERR_INVALID_ARGUMENT;
+  for (int i = 0; i < n; ++i)
+    if (pkv::overlap(payload, pb, caches[i].p, caches[i].n) || pkv::overlap(scales, sb, caches[i].p, caches[i].n))
+      return PKV_ERR_INVALID_ARGUMENT;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
 
@@ -598,7 +602,8 @@ pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, co
   a.v_cache = static_cast<const uint16_t*>(v_cache);
   a.payload = static_cast<uint8_t*>(payload);
   a.scales = static_cast<uint16_t*>(scales);
-  a.layer_elems = m.pool_pages * int64_t(m.page_size) * m.num_kv_heads * m.head_dim;
+  a.layer_elems = pkv::layer_elems(m);
+  a.page_shift = pkv::page_shift(m);
   a.H = m.num_kv_heads;
   a.D = m.head_dim;
   a.B = m.block_tokens;

@@ -141,6 +141,25 @@ uint64_t layer_payload_bytes(const pkv_model_t& m, const uint8_t* tags, int64_t 
 // Tokens per unit for a model: about kUnitElems output elements, at most one block.
 int32_t unit_tokens(const pkv_model_t& m);
 
+// Cache geometry by layout.  A page's slots start at page << page_shift slot
+// rows from the layer's start (log2 P, plus one when a page holds its K and V
+// slots back to back); a layer spans layer_elems elements of either cache.
+int32_t page_shift(const pkv_model_t& m);
+int64_t layer_elems(const pkv_model_t& m);
+uint64_t cache_bytes(const pkv_model_t& m);  // of each separate cache, or of the paired one
+
+// The cache pointers of a call against the model's layout: both 16-byte
+// aligned; separate caches of cache_bytes each must not overlap; a paired
+// cache has v_cache = k_cache + P*H*D elements.  `ranges` receives the byte
+// ranges the caches occupy (two, or one for a paired cache) for overlap
+// checks against other buffers; returns false on a bad placement.
+struct ByteRange {
+  const void* p;
+  uint64_t n;
+};
+bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache, uint64_t bytes, ByteRange (&ranges)[2],
+                  int& count);
+
 }  // namespace pkv
 
 #endif  // PKV_INTERNAL_H

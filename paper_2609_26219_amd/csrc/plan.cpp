@@ -42,13 +42,15 @@ pkv_status_t check_model(const pkv_model_t* m) {
   if (m->rope_style != PKV_ROPE_HALF && m->rope_style != PKV_ROPE_INTERLEAVED) return PKV_ERR_INVALID_ARGUMENT;
   if (m->rotary_dim != 0 && (m->rotary_dim < 16 || m->rotary_dim > m->head_dim || m->rotary_dim % 16 != 0))
     return PKV_ERR_INVALID_ARGUMENT;
+  if (m->kv_layout != PKV_KV_SEPARATE && m->kv_layout != PKV_KV_PAIRED) return PKV_ERR_INVALID_ARGUMENT;
+  if (m->reserved != 0) return PKV_ERR_INVALID_ARGUMENT;
   if (m->inv_freq) {
     const int32_t R = m->rotary_dim ? m->rotary_dim : m->head_dim;
     for (int32_t i = 0; i < R / 2; ++i)
       if (!isfinite(m->inv_freq[i])) return PKV_ERR_INVALID_ARGUMENT;
   }
   // Cache elements per layer and in total must stay far from int64 overflow.
-  const double elems = double(m->num_layers) * double(m->pool_pages) * m->page_size * m->num_kv_heads * m->head_dim;
+  const double elems = 2.0 * double(m->num_layers) * double(m->pool_pages) * m->page_size * m->num_kv_heads * m->head_dim;
   if (elems > 1e18) return PKV_ERR_INVALID_ARGUMENT;
   return PKV_OK;
 }
@@ -97,6 +99,31 @@ uint64_t tile_bytes(const pkv_model_t& m, int bits) {
 }
 
 }  // namespace
+
+int32_t page_shift(const pkv_model_t& m) { return ilog2(m.page_size) + (m.kv_layout == PKV_KV_PAIRED ? 1 : 0); }
+
+int64_t layer_elems(const pkv_model_t& m) {
+  return (m.kv_layout == PKV_KV_PAIRED ? 2 : 1) * m.pool_pages * int64_t(m.page_size) * m.num_kv_heads * m.head_dim;
+}
+
+uint64_t cache_bytes(const pkv_model_t& m) { return uint64_t(m.num_layers) * uint64_t(layer_elems(m)) * 2; }
+
+bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache, uint64_t bytes, ByteRange (&ranges)[2],
+                  int& count) {
+  const uintptr_t k = reinterpret_cast<uintptr_t>(k_cache), v = reinterpret_cast<uintptr_t>(v_cache);
+  if (k % 16 || v % 16) return false;
+  if (m.kv_layout == PKV_KV_PAIRED) {
+    if (v != k + uint64_t(m.page_size) * m.num_kv_heads * m.head_dim * 2) return false;
+    ranges[0] = ByteRange{k_cache, bytes};
+    count = 1;
+    return true;
+  }
+  if (k < v + bytes && v < k + bytes) return false;
+  ranges[0] = ByteRange{k_cache, bytes};
+  ranges[1] = ByteRange{v_cache, bytes};
+  count = 2;
+  return true;
+}
 
 int32_t unit_tokens(const pkv_model_t& m) {
   const int64_t per = kUnitElems / (int64_t(m.num_kv_heads) * m.head_dim);
@@ -165,7 +192,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
   hp.page_tables.clear();
   memset(&hp.info, 0, sizeof(hp.info));
   hp.info.num_requests = num_requests;
-  hp.info.cache_bytes = uint64_t(L) * uint64_t(m.pool_pages) * uint64_t(P) * uint64_t(H) * uint64_t(D) * 2;
+  hp.info.cache_bytes = cache_bytes(m);
 
   if (int64_t(num_requests) * D > std::numeric_limits<int32_t>::max()) return PKV_ERR_INVALID_ARGUMENT;
   try {
@@ -244,8 +271,11 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
           if (q.repair_mask[b]) continue;
           const int tag = q.tags[b];
           const int64_t n_valid = std::min<int64_t>(B, q.suffix_tokens - b * B);
-          // Split the block into units of at most `per_unit` tokens.
-          for (int64_t t0 = 0; t0 < n_valid; t0 += per_unit) {
+          // Split the block into units of at most `per_unit` tokens that
+          // never cross a page boundary, so a unit writes slots of one page.
+          for (int64_t t0 = 0, len = 0; t0 < n_valid; t0 += len) {
+            const int64_t to_page_end = P - ((q.dst_row0 + b * B + t0) & (P - 1));
+            len = std::min<int64_t>(std::min<int64_t>(per_unit, to_page_end), n_valid - t0);
             Unit u;
             const uint64_t block_base = layer_base + block_off[r][b];
             u.k_off = block_base + uint64_t(t0) * H * D * kKeyBits[tag] / 8;
@@ -256,7 +286,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
             u.table_off = int32_t(rd.table_off);
             u.layer = int32_t(l);
             u.tag = tag | (q.delta != 0 ? kUnitRotate : 0);
-            u.n_valid = int32_t(std::min<int64_t>(per_unit, n_valid - t0));
+            u.n_valid = int32_t(len);
             u.page1 = 0;
             u.page2 = 0;
             hp.units.push_back(u);
@@ -348,7 +378,7 @@ pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoin
   memset(&hp.info, 0, sizeof(hp.info));
   hp.info.num_requests = num_requests;
   hp.info.kind = 1;
-  hp.info.cache_bytes = uint64_t(L) * uint64_t(m.pool_pages) * uint64_t(P) * uint64_t(H) * uint64_t(D) * 2;
+  hp.info.cache_bytes = cache_bytes(m);
   try {
     for (int32_t r = 0; r < num_requests; ++r) {
       const pkv_checkpoint_request_t& q = requests[r];

@@ -48,9 +48,10 @@ struct KernelArgs {
   const uint16_t* scales;
   uint16_t* k_cache;
   uint16_t* v_cache;
-  int64_t layer_elems;  // pool_pages * P * H * D
+  int64_t layer_elems;  // elements of one layer of a cache: pool_pages * P * H * D, twice that when paired
   int32_t H, D, log2P, cols, tpp;
   int32_t R;            // rotary channels per head
+  int32_t page_shift;   // slot rows from a layer's start to page p: p << page_shift
 };
 
 __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
@@ -193,14 +194,11 @@ __device__ __forceinline__ void decode_run(const Chunk8<KBITS>& c, float s, floa
   for (int e = 0; e < 8; ++e) out[e] = decode_f<KBITS>(c, e, s, z);
 }
 
-// Keys of one (token, head), piece p.
+// Keys of one (token, head), piece p, from its two loaded runs: decode,
+// rotate, round, store.
 template <int KBITS, bool ROT, int STYLE, bool BF16>
-__device__ __forceinline__ void restore_key_piece(const uint8_t* __restrict__ row, const KeyPiece& p, float ks,
-                                                  float kz, const double2* __restrict__ cs,
-                                                  uint16_t* __restrict__ dst) {
-  Chunk8<KBITS> lo, hi;
-  lo.load(row + p.lo * KBITS / 8);
-  hi.load(row + p.hi * KBITS / 8);
+__device__ __forceinline__ void key_store(const Chunk8<KBITS>& lo, const Chunk8<KBITS>& hi, const KeyPiece& p, float ks,
+                                          float kz, const double2* __restrict__ cs, uint16_t* __restrict__ dst) {
   uint4 out_lo, out_hi;
   if constexpr (KBITS == 16 && !ROT && !BF16) {
     // binary16 in, binary16 out, no rotation: the bits are the result.
@@ -242,13 +240,10 @@ __device__ __forceinline__ void restore_key_piece(const uint8_t* __restrict__ ro
   store_row_piece(dst + p.hi, out_hi);
 }
 
-// Values of one (token, head): the same piece j; never rotated.
+// Values of one (token, head), piece j (never rotated).
 template <int VBITS, bool BF16>
-__device__ __forceinline__ void restore_value_piece(const uint8_t* __restrict__ row, int j, int D, float vs, float vz,
-                                                    uint16_t* __restrict__ dst) {
-  Chunk8<VBITS> lo, hi;
-  lo.load(row + (8 * j) * VBITS / 8);
-  hi.load(row + (D / 2 + 8 * j) * VBITS / 8);
+__device__ __forceinline__ void value_store(const Chunk8<VBITS>& lo, const Chunk8<VBITS>& hi, int j, int D, float vs,
+                                            float vz, uint16_t* __restrict__ dst) {
   uint4 out_lo, out_hi;
   if constexpr (VBITS == 16 && !BF16) {
     out_lo = lo.w;
@@ -267,40 +262,92 @@ __device__ __forceinline__ void restore_value_piece(const uint8_t* __restrict__ 
   store_row_piece(dst + D / 2 + 8 * j, out_hi);
 }
 
-template <int TAG, bool ROT, int STYLE, bool BF16>
-__device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u, const double* __restrict__ s_tab,
-                                             int t0, int head, int j) {
+// What a thread needs for every token of its unit.
+struct Piece {
+  int head, j;
+  KeyPiece kp;
+  float ks, kz, vs, vz;
+  int64_t lbase;  // cache element offset of the unit's layer and the thread's head
+};
+
+// NK tokens of one thread (t, t + tpp, ...): every load is issued before the
+// first store, so a wave keeps NK tokens of payload in flight.
+template <int NK, int TAG, bool ROT, int STYLE, bool BF16>
+__device__ __forceinline__ void restore_tokens(const KernelArgs& a, const Unit& u, int t, const Piece& q,
+                                               const double2* __restrict__ cs) {
   constexpr int KB = kKeyBits[TAG];
   constexpr int VB = kValueBits[TAG];
   const int H = a.H, D = a.D;
-  float ks = 0.f, kz = 0.f, vs = 0.f, vz = 0.f;
+  const uint8_t* kbase = a.payload + u.k_off;
+  const uint8_t* vbase = a.payload + u.v_off;
+  const int64_t slot_mask = (int64_t(1) << a.log2P) - 1;
+  const int64_t row_elems = int64_t(H) * D;
+  Chunk8<KB> klo[NK], khi[NK];
+  Chunk8<VB> vlo[NK], vhi[NK];
+  int64_t dst[NK];
+#pragma unroll
+  for (int k = 0; k < NK; ++k) {
+    const int tk = t + k * a.tpp;
+    const int64_t row = u.row0 + tk;
+    const int64_t page = a.page_tables[u.pt_off + (row >> a.log2P)];
+    dst[k] = q.lbase + ((page << a.page_shift) | (row & slot_mask)) * row_elems;
+    const int64_t r = int64_t(tk) * H + q.head;
+    klo[k].load(kbase + r * (D * KB / 8) + q.kp.lo * KB / 8);
+    khi[k].load(kbase + r * (D * KB / 8) + q.kp.hi * KB / 8);
+    vlo[k].load(vbase + r * (D * VB / 8) + (8 * q.j) * VB / 8);
+    vhi[k].load(vbase + r * (D * VB / 8) + (D / 2 + 8 * q.j) * VB / 8);
+  }
+#pragma unroll
+  for (int k = 0; k < NK; ++k) {
+    key_store<KB, ROT, STYLE, BF16>(klo[k], khi[k], q.kp, q.ks, q.kz, cs, a.k_cache + dst[k]);
+    value_store<VB, BF16>(vlo[k], vhi[k], q.j, D, q.vs, q.vz, a.v_cache + dst[k]);
+  }
+}
+
+template <int TAG, bool ROT, int STYLE, bool BF16>
+__device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u, const double* __restrict__ s_tab,
+                                             int t0, int head, int j) {
+  Piece q;
+  q.head = head;
+  q.j = j;
+  q.kp = key_piece<STYLE>(j, a.D, a.R);
+  q.ks = q.kz = q.vs = q.vz = 0.f;
   if constexpr (TAG != PKV_TAG_FP16) {
     const uint2 sw = *reinterpret_cast<const uint2*>(a.scales + u.scale_off + 4 * head);
-    ks = half_bits_to_float(sw.x & 0xFFFFu);
-    kz = half_bits_to_float(sw.x >> 16);
-    vs = half_bits_to_float(sw.y & 0xFFFFu);
-    vz = half_bits_to_float(sw.y >> 16);
+    q.ks = half_bits_to_float(sw.x & 0xFFFFu);
+    q.kz = half_bits_to_float(sw.x >> 16);
+    q.vs = half_bits_to_float(sw.y & 0xFFFFu);
+    q.vz = half_bits_to_float(sw.y >> 16);
   }
+  q.lbase = int64_t(u.layer) * a.layer_elems + int64_t(head) * a.D;
   double2 cs[8];  // (cos, sin) of this thread's eight rotary pairs
   if constexpr (ROT) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) cs[e] = *reinterpret_cast<const double2*>(s_tab + 2 * (8 * j + e));
   }
-  const uint8_t* kbase = a.payload + u.k_off;
-  const uint8_t* vbase = a.payload + u.v_off;
-  const int64_t krow_bytes = int64_t(D) * KB / 8, vrow_bytes = int64_t(D) * VB / 8;
-  const int64_t slot_mask = (int64_t(1) << a.log2P) - 1;
-  const int64_t row_elems = int64_t(H) * D;
-  const int64_t lbase = int64_t(u.layer) * a.layer_elems + int64_t(head) * D;
-  const KeyPiece kp = key_piece<STYLE>(j, D, a.R);
-  for (int t = t0; t < u.n_valid; t += a.tpp) {
-    const int64_t row = u.row0 + t;
-    const int64_t page = a.page_tables[u.pt_off + (row >> a.log2P)];
-    const int64_t dst = lbase + ((page << a.log2P) | (row & slot_mask)) * row_elems;
-    const int64_t r = int64_t(t) * H + head;
-    restore_key_piece<KB, ROT, STYLE, BF16>(kbase + r * krow_bytes, kp, ks, kz, cs, a.k_cache + dst);
-    restore_value_piece<VB, BF16>(vbase + r * vrow_bytes, j, D, vs, vz, a.v_cache + dst);
+  // A unit holds at most 4 * tpp tokens when H*D divides 4096, so a thread
+  // has at most four; FP16 runs them two at a time (16-byte runs take twice
+  // the registers).  Other shapes take the remaining tokens one by one.
+  const int nk = t0 < u.n_valid ? (u.n_valid - t0 + a.tpp - 1) / a.tpp : 0;
+  if constexpr (TAG != PKV_TAG_FP16) {
+    switch (nk) {
+      case 0: return;
+      case 1: restore_tokens<1, TAG, ROT, STYLE, BF16>(a, u, t0, q, cs); return;
+      case 2: restore_tokens<2, TAG, ROT, STYLE, BF16>(a, u, t0, q, cs); return;
+      case 3: restore_tokens<3, TAG, ROT, STYLE, BF16>(a, u, t0, q, cs); return;
+      case 4: restore_tokens<4, TAG, ROT, STYLE, BF16>(a, u, t0, q, cs); return;
+      default: break;
+    }
+  } else if (nk <= 4) {
+    for (int k = nk, t = t0; k > 0; k -= 2, t += 2 * a.tpp) {
+      if (k >= 2)
+        restore_tokens<2, TAG, ROT, STYLE, BF16>(a, u, t, q, cs);
+      else
+        restore_tokens<1, TAG, ROT, STYLE, BF16>(a, u, t, q, cs);
+    }
+    return;
   }
+  for (int t = t0; t < u.n_valid; t += a.tpp) restore_tokens<1, TAG, ROT, STYLE, BF16>(a, u, t, q, cs);
 }
 
 template <bool BF16, int STYLE>
@@ -431,16 +478,17 @@ pkv_status_t check_restore_buffers(const pkv_plan* plan, const void* payload, ui
                                    uint64_t cache_bytes) {
   const pkv_plan_info_t& info = plan->host.info;
   if (!payload || !scales || !k_cache || !v_cache) return PKV_ERR_INVALID_ARGUMENT;
-  if (reinterpret_cast<uintptr_t>(payload) % 16 || reinterpret_cast<uintptr_t>(scales) % 8 ||
-      reinterpret_cast<uintptr_t>(k_cache) % 16 || reinterpret_cast<uintptr_t>(v_cache) % 16)
+  if (reinterpret_cast<uintptr_t>(payload) % 16 || reinterpret_cast<uintptr_t>(scales) % 8)
     return PKV_ERR_INVALID_ARGUMENT;
   if (payload_bytes < info.payload_bytes || scale_bytes < info.scale_bytes || cache_bytes < info.cache_bytes)
     return PKV_ERR_INVALID_ARGUMENT;
-  const uint64_t cb = info.cache_bytes;
-  if (ranges_overlap(k_cache, cb, v_cache, cb) || ranges_overlap(k_cache, cb, payload, info.payload_bytes) ||
-      ranges_overlap(v_cache, cb, payload, info.payload_bytes) || ranges_overlap(k_cache, cb, scales, info.scale_bytes) ||
-      ranges_overlap(v_cache, cb, scales, info.scale_bytes))
-    return PKV_ERR_INVALID_ARGUMENT;
+  ByteRange caches[2];
+  int n = 0;
+  if (!cache_ranges(plan->host.model, k_cache, v_cache, info.cache_bytes, caches, n)) return PKV_ERR_INVALID_ARGUMENT;
+  for (int i = 0; i < n; ++i)
+    if (ranges_overlap(caches[i].p, caches[i].n, payload, info.payload_bytes) ||
+        ranges_overlap(caches[i].p, caches[i].n, scales, info.scale_bytes))
+      return PKV_ERR_INVALID_ARGUMENT;
   return PKV_OK;
 }
 
@@ -456,7 +504,8 @@ pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const voi
   a.scales = static_cast<const uint16_t*>(scales);
   a.k_cache = static_cast<uint16_t*>(k_cache);
   a.v_cache = static_cast<uint16_t*>(v_cache);
-  a.layer_elems = m.pool_pages * int64_t(m.page_size) * m.num_kv_heads * m.head_dim;
+  a.layer_elems = layer_elems(m);
+  a.page_shift = page_shift(m);
   a.H = m.num_kv_heads;
   a.D = m.head_dim;
   a.log2P = plan->host.log2_page;

@@ -72,13 +72,29 @@ def suffix_rows(case: wl.Case, layers: Sequence[int], workers: Optional[int] = N
             pool.join()
 
 
-def _scatter_rows(cache_layer, slots, bits):
+def alloc_caches(shape, device, fill: Optional[int] = None):
+    """K and V caches of ``shape`` on the device, each seen as
+    ``[L][pool_pages][P][H][D]`` int16: two tensors (``KV_SEPARATE``), or the
+    K and V views ``[:, :, 0]`` / ``[:, :, 1]`` of one
+    ``[L][pool_pages][2][P][H][D]`` tensor (``KV_PAIRED``)."""
     import torch
 
-    s = cache_layer.shape
-    flat = cache_layer.view(-1, s[-2], s[-1])
-    idx = torch.from_numpy(slots).to(cache_layer.device)
-    flat.index_copy_(0, idx, torch.from_numpy(bits.view(np.int16)).to(cache_layer.device))
+    dims = (shape.num_layers, shape.pool_pages, shape.page_size, shape.num_kv_heads, shape.head_dim)
+    make = (lambda d: torch.empty(d, dtype=torch.int16, device=device)) if fill is None else \
+        (lambda d: torch.full(d, fill, dtype=torch.int16, device=device))
+    if getattr(shape, "kv_layout", wl.KV_SEPARATE) == wl.KV_PAIRED:
+        kv = make(dims[:2] + (2,) + dims[2:])
+        return kv[:, :, 0], kv[:, :, 1]
+    return make(dims), make(dims)
+
+
+def _scatter_rows(cache_layer, slots, bits):
+    """Write rows ``bits`` ``[n, H, D]`` into slots of one layer ``[pool_pages][P][H][D]``."""
+    import torch
+
+    P = cache_layer.shape[1]
+    idx = torch.from_numpy(np.asarray(slots, dtype=np.int64)).to(cache_layer.device)
+    cache_layer[idx // P, idx % P] = torch.from_numpy(bits.view(np.int16)).to(cache_layer.device)
 
 
 class OldCaches:
@@ -89,11 +105,9 @@ class OldCaches:
 
         self.case = case
         s = case.src_shape
-        shape = (s.num_layers, s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim)
         nan = wl.cache_nan_bits(s.out_dtype)
         nan = nan - 65536 if nan >= 32768 else nan
-        self.k = torch.full(shape, nan, dtype=torch.int16, device=device)
-        self.v = torch.full(shape, nan, dtype=torch.int16, device=device)
+        self.k, self.v = alloc_caches(s, device, nan)
         for ri, layer, (slots, kb, vb) in suffix_rows(case, range(s.num_layers), workers):
             _scatter_rows(self.k[layer], slots, kb)
             _scatter_rows(self.v[layer], slots, vb)
@@ -130,11 +144,9 @@ def write_checkpoint_layerwise(case: wl.Case, payload, scales, device: str = "cu
     import torch
 
     s1 = dataclasses.replace(case.src_shape, num_layers=1)
-    shape = (1, s1.pool_pages, s1.page_size, s1.num_kv_heads, s1.head_dim)
     nan = wl.cache_nan_bits(s1.out_dtype)
     nan = nan - 65536 if nan >= 32768 else nan
-    k = torch.empty(shape, dtype=torch.int16, device=device)
-    v = torch.empty(shape, dtype=torch.int16, device=device)
+    k, v = alloc_caches(s1, device)
     current = None
     rows = []
 
@@ -186,9 +198,7 @@ class DeviceRestore:
             else:
                 self.payload.copy_(p)
                 self.scales.copy_(sc)
-        cache_shape = (s.num_layers, s.pool_pages, s.page_size, s.num_kv_heads, s.head_dim)
-        self.k_cache = torch.empty(cache_shape, dtype=torch.int16, device=self.device)
-        self.v_cache = torch.empty(cache_shape, dtype=torch.int16, device=self.device)
+        self.k_cache, self.v_cache = alloc_caches(s, self.device)
         self.prefill()
         self.plan = binding.pkv_restore_plan(s, case.requests)
         self.info = binding.pkv_plan_query(self.plan)
@@ -197,13 +207,17 @@ class DeviceRestore:
         """Fill both caches with the generator's position-dependent pattern."""
         import torch
 
+        s = self.case.shape
+        page = s.page_size * s.row_elems
+        pages_per_chunk = max(1, _CHUNK // page)
         for which, cache in ((0, self.k_cache), (1, self.v_cache)):
-            flat = cache.view(-1)
             seed = self.case.prefill_seed(which)
-            for start in range(0, flat.numel(), _CHUNK):
-                end = min(flat.numel(), start + _CHUNK)
-                idx = torch.arange(start, end, dtype=torch.int64, device=self.device)
-                flat[start:end] = _to_int16(wl.prefill_bits_torch(idx, seed))
+            for layer in range(s.num_layers):
+                for p0 in range(0, s.pool_pages, pages_per_chunk):
+                    p1 = min(s.pool_pages, p0 + pages_per_chunk)
+                    start = layer * s.layer_elems + p0 * page
+                    idx = torch.arange(start, start + (p1 - p0) * page, dtype=torch.int64, device=self.device)
+                    cache[layer, p0:p1] = _to_int16(wl.prefill_bits_torch(idx, seed)).view(cache[layer, p0:p1].shape)
         torch.cuda.synchronize(self.device)
 
     def run(self, stream=None) -> None:
@@ -218,17 +232,19 @@ class DeviceRestore:
         row = s.row_elems
         keep = torch.from_numpy(~written_slots).to(self.device)
         bad = 0
+        P = s.page_size
+        pages_per_chunk = max(1, _CHUNK // (P * row))
         for which, cache in ((0, self.k_cache), (1, self.v_cache)):
             seed = self.case.prefill_seed(which)
-            flat = cache.view(s.num_layers, s.pool_slots, row)
-            slots_per_chunk = max(1, _CHUNK // row)
             for layer in range(s.num_layers):
                 base = layer * s.layer_elems
-                for s0 in range(0, s.pool_slots, slots_per_chunk):
-                    s1 = min(s.pool_slots, s0 + slots_per_chunk)
+                for p0 in range(0, s.pool_pages, pages_per_chunk):
+                    p1 = min(s.pool_pages, p0 + pages_per_chunk)
+                    s0, s1 = p0 * P, p1 * P
                     idx = torch.arange(base + s0 * row, base + s1 * row, dtype=torch.int64, device=self.device)
                     want = _to_int16(wl.prefill_bits_torch(idx, seed)).view(s1 - s0, row)
-                    diff = (flat[layer, s0:s1] != want) & keep[s0:s1, None]
+                    got = cache[layer, p0:p1].reshape(s1 - s0, row)
+                    diff = (got != want) & keep[s0:s1, None]
                     bad += int(diff.sum().item())
         return bad
 
@@ -237,10 +253,11 @@ class DeviceRestore:
         import torch
 
         cache = self.k_cache if which == 0 else self.v_cache
-        s = self.case.shape
-        flat = cache.view(s.num_layers, s.pool_slots, s.num_kv_heads, s.head_dim)
+        P = self.case.shape.page_size
         idx = torch.from_numpy(np.asarray(slots, dtype=np.int64)).to(self.device)
-        return flat[layer].index_select(0, idx).cpu().numpy().view(np.uint16)
+        return cache[layer][idx // P, idx % P].cpu().numpy().view(np.uint16)
 
     def host_caches(self):
-        return (self.k_cache.cpu().numpy().view(np.uint16), self.v_cache.cpu().numpy().view(np.uint16))
+        """Both caches on the host, ``[L][pool_pages][P][H][D]`` uint16 each, whatever the device layout."""
+        return (self.k_cache.contiguous().cpu().numpy().view(np.uint16),
+                self.v_cache.contiguous().cpu().numpy().view(np.uint16))

@@ -36,6 +36,7 @@ TAG_NAMES = ("FP16", "K8V8", "K8V4", "K4V4")
 KEY_BITS = (16, 8, 8, 4)
 VALUE_BITS = (16, 8, 4, 4)
 OUT_FP16, OUT_BF16 = 0, 1
+KV_SEPARATE, KV_PAIRED = 0, 1  # device cache layouts (pkv_kv_layout_t)
 
 FP16_NAN_BITS = 0x7E00
 
@@ -62,6 +63,7 @@ class Shape:
     rope_style: int = 0  # ROPE_HALF or ROPE_INTERLEAVED
     rotary_dim: int = 0  # 0 = head_dim
     inv_freq: Optional[Tuple[float, ...]] = None  # explicit pair frequencies, else theta^(-2i/rotary_dim)
+    kv_layout: int = 0  # KV_SEPARATE or KV_PAIRED (device caches only; host caches are always two arrays)
 
     @property
     def pool_slots(self) -> int:

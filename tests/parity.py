@@ -316,10 +316,13 @@ def gpu_checkpoint(case, torch, caches=None):
     unless given); payload and scales start filled with marker values."""
     from paper_2609_26219_amd import binding as pb
 
+    from paper_2609_26219_amd.device import alloc_caches
+
     s = case.src_shape
     kc, vc = case.host_old_caches() if caches is None else caches
-    dk = torch.from_numpy(kc.view(np.int16)).cuda()
-    dv = torch.from_numpy(vc.view(np.int16)).cuda()
+    dk, dv = alloc_caches(s, "cuda")  # in the shape's layout
+    dk.copy_(torch.from_numpy(kc.view(np.int16)))
+    dv.copy_(torch.from_numpy(vc.view(np.int16)))
     payload = torch.full((case.payload_nbytes,), FILL, dtype=torch.uint8, device="cuda")
     scales = torch.full((case.scale_elems,), 0x5A5A, dtype=torch.int16, device="cuda")
     plan = pb.pkv_checkpoint_plan(s, case.requests)

@@ -2,8 +2,8 @@
 field drawn over its valid range (head_dim, heads, block and page sizes,
 layers, several requests with partial blocks and unaligned first rows, zero,
 small and large shifts, tag subsets, repair fractions, output dtypes, both
-RoPE pairings, partial rotary dimensions and scaled frequency tables), sized
-so that the oracle finishes each in seconds."""
+RoPE pairings, partial rotary dimensions, scaled frequency tables and both
+cache layouts), sized so that the oracle finishes each in seconds."""
 import dataclasses
 
 import numpy as np
@@ -40,8 +40,9 @@ def sweep_case(i: int) -> "wl.Case":
     style = int(r.integers(0, 2))
     R = int(16 * r.integers(1, D // 16 + 1))
     scaled = bool(r.random() < 0.3)
+    layout = int(r.integers(0, 2))
     case.shape = dataclasses.replace(case.shape, rope_style=style, rotary_dim=0 if R == D else R,
-                                     inv_freq=wl.llama3_inv_freq(theta, R) if scaled else None)
+                                     inv_freq=wl.llama3_inv_freq(theta, R) if scaled else None, kv_layout=layout)
     return case
 
 
@@ -50,6 +51,7 @@ def describe(case) -> str:
     return (f"L{s.num_layers} H{s.num_kv_heads} D{s.head_dim} B{s.block_tokens} P{s.page_size} "
             f"out={'bf16' if s.out_dtype else 'fp16'} rope={'interleaved' if s.rope_style else 'half'} "
             f"R={s.rotary_dim or s.head_dim} scaled={s.inv_freq is not None} theta={s.rope_theta:g} "
+            f"kv={'paired' if s.kv_layout else 'separate'} "
             f"reqs={[(q.suffix_tokens, q.delta, q.dst_row0) for q in case.requests]} "
             f"tags={sorted(set(int(t) for q in case.requests for t in q.tags))}")
 
@@ -66,5 +68,8 @@ LIMIT_CASES = {
 
 
 def limit_case(name: str) -> "wl.Case":
-    return wl.make_custom(77, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2, out_dtype=wl.OUT_BF16,
+    case = wl.make_custom(77, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2, out_dtype=wl.OUT_BF16,
                           outlier_pairs=1, **LIMIT_CASES[name])
+    if name.startswith("b1024"):  # the largest blocks on paired pages too
+        case.shape = dataclasses.replace(case.shape, kv_layout=wl.KV_PAIRED)
+    return case

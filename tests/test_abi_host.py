@@ -97,6 +97,7 @@ def test_valid_plan_passes_validation():
     ("head_dim", 72), ("head_dim", 8), ("head_dim", 1024), ("num_kv_heads", 0), ("num_layers", 0),
     ("page_size", 12), ("page_size", 0), ("pool_pages", 0), ("rope_theta", 0.0), ("rope_theta", float("nan")),
     ("out_dtype", 2), ("block_tokens", 0), ("block_tokens", 2048), ("num_kv_heads", 65),
+    ("kv_layout", 2), ("kv_layout", -1),
 ])
 def test_bad_model(field, value):
     shape, reqs = _base()
@@ -306,3 +307,22 @@ def test_missing_library_fails_loudly():
             pb.load("/nonexistent/libpkv.so")
     finally:
         pb._lib = saved
+
+
+def test_model_reserved_field_must_be_zero():
+    import ctypes
+    shape, reqs = _base()
+    m = pb.make_model(shape)
+    m.reserved = 1
+    units_fn = pb.load().pkv_payload_size
+    size, elems = ctypes.c_uint64(), ctypes.c_uint64()
+    r = pb._Requests(reqs)
+    assert units_fn(ctypes.byref(m), r.array, ctypes.byref(size), ctypes.byref(elems)) == pb.PKV_ERR_INVALID_ARGUMENT
+    m.reserved = 0
+    assert units_fn(ctypes.byref(m), r.array, ctypes.byref(size), ctypes.byref(elems)) == pb.PKV_OK
+
+
+def test_paired_layout_is_a_valid_model():
+    import dataclasses
+    shape, reqs = _base()
+    assert _status(dataclasses.replace(shape, kv_layout=wl.KV_PAIRED), reqs) == VALID

@@ -45,6 +45,18 @@ def test_checkpoint_bit_exact_custom(params, torch):
     check_checkpoint_write(case, torch)
 
 
+@pytest.mark.parametrize("params", [
+    dict(L=2, H=2, D=64, B=16, P=16, n_tokens=(100, 40), deltas=(5, -3), rho0s=(20, 7), out_dtype=wl.OUT_BF16),
+    dict(L=2, H=8, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,), out_dtype=wl.OUT_BF16),
+    dict(L=1, H=4, D=64, B=32, P=8, n_tokens=(77,), deltas=(1,), rho0s=(6,), out_dtype=wl.OUT_FP16),
+], ids=["two_requests", "h8_d128", "general_kernel"])
+def test_checkpoint_bit_exact_paired_pages(params, torch):
+    import dataclasses
+    case = wl.make_custom(12, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), outlier_pairs=1, **params)
+    case.shape = dataclasses.replace(case.shape, kv_layout=wl.KV_PAIRED)
+    check_checkpoint_write(case, torch)
+
+
 @pytest.mark.parametrize("out", [wl.OUT_FP16, wl.OUT_BF16])
 def test_checkpoint_exact_and_near_ties(out, torch):
     """Rows on a grid of half-integer multiples of the scale (exact ties, which

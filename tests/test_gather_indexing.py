@@ -58,7 +58,10 @@ def emulate(case):
     nload = -(-B // rpl)
     NL = loads_per_chunk(nload)
     nchunk = -(-nload // NL)
-    layer_elems = s.pool_pages * P * H * D
+    paired = s.kv_layout == wl.KV_PAIRED
+    shift = int(np.log2(P)) + int(paired)  # slot rows from a layer's start to page p: p << shift
+    layer_elems = (2 if paired else 1) * s.pool_pages * P * H * D
+    v_offset = P * H * D if paired else 0  # V reads in the one paired buffer; separate caches share cache_read
     cache_read = np.zeros(L * layer_elems, dtype=np.int32)
     pw = np.zeros(case.payload_nbytes, dtype=np.int32)
     sw = np.zeros(case.scale_elems, dtype=np.int32)
@@ -81,7 +84,8 @@ def emulate(case):
                             rows = int(u["row0"]) + t[rd]
                             pages = pt_all[int(u["pt_off"]) + rows // P]
                             assert ((pages >= 0) & (pages < s.pool_pages)).all()
-                            base = int(u["layer"]) * layer_elems + (pages * P + rows % P) * H * D + head * D + 8 * c[rd]
+                            base = (int(u["layer"]) * layer_elems + ((pages << shift) | (rows % P)) * H * D + head * D
+                                    + 8 * c[rd] + which * v_offset)
                             for e in range(8):
                                 np.add.at(cache_read, base + e, passes)
                             wr = on & (t < B)
@@ -113,12 +117,12 @@ def emulate(case):
             tag = int(r_.tags[b])
             n = min(B, r_.suffix_tokens - b * B)
             rows = r_.src_row0 + b * B + np.arange(n)
-            slots = r_.src_page_table[rows // P].astype(np.int64) * P + rows % P
+            slot_rows = (r_.src_page_table[rows // P].astype(np.int64) << shift) | (rows % P)
             for layer in range(L):
                 for which, bits in enumerate((KBITS[tag], VBITS[tag])):
                     k = 1 if bits == 16 or nchunk == 1 else 2
-                    for sl in slots:
-                        b0 = layer * layer_elems + sl * H * D
+                    for sl in slot_rows:
+                        b0 = layer * layer_elems + sl * H * D + which * v_offset
                         want_r[b0: b0 + H * D] += k
     assert np.array_equal(cache_read, want_r)
 
@@ -144,6 +148,26 @@ def emulate(case):
 ], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "h4_b64", "h8_d128", "d48_idle_lanes",
         "d512_two_chunks", "h20_heads_loop"])
 def test_gather_addresses(maker):
+    emulate(maker())
+
+
+def _paired(case):
+    import dataclasses
+    case.shape = dataclasses.replace(case.shape, kv_layout=wl.KV_PAIRED)
+    return case
+
+
+@pytest.mark.parametrize("maker", [
+    lambda: _paired(wl.make_case("tiny")),
+    lambda: _paired(wl.make_custom(2, L=1, H=8, D=64, B=4, P=16, n_tokens=(23, 9), deltas=(5, 0), rho0s=(7, 40),
+                                   tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1))),
+    lambda: _paired(wl.make_custom(5, L=2, H=8, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,),
+                                   tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1))),
+    # general kernel: blocks over more than three pages
+    lambda: _paired(wl.make_custom(9, L=1, H=4, D=64, B=32, P=8, n_tokens=(77,), deltas=(1,), rho0s=(6,),
+                                   tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1))),
+], ids=["tiny", "h8_b4_two_requests", "h8_d128", "general_kernel"])
+def test_gather_addresses_paired_pages(maker):
     emulate(maker())
 
 

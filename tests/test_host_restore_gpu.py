@@ -53,6 +53,12 @@ def _check_copied_only_reused(case, dr, ckpt):
         f"in {info['host_copies']} copies")
 
 
+def _paired(case):
+    import dataclasses
+    case.shape = dataclasses.replace(case.shape, kv_layout=wl.KV_PAIRED)
+    return case
+
+
 CASES = [
     ("tiny", lambda: wl.make_case("tiny")),
     ("llama8b_1l", lambda: wl.make_case("llama8b_1l")),
@@ -60,6 +66,7 @@ CASES = [
                                                  deltas=(3, 0, -7), rho0s=(0, 6, 13), tag_set=(0, 1, 2, 3),
                                                  mix=(1, 1, 1, 1), repair_frac=0.3, out_dtype=wl.OUT_BF16,
                                                  outlier_pairs=1)),
+    ("llama8b_1l_paired_pages", lambda: _paired(wl.make_case("llama8b_1l"))),
 ]
 
 

@@ -47,8 +47,11 @@ def emulate(case):
     cols = H * D // 16
     tpp = WG // cols
     dq = D // 16
-    layer_elems = s.pool_pages * P * H * D
-    cache_elems = s.num_layers * layer_elems
+    paired = s.kv_layout == wl.KV_PAIRED
+    shift = int(np.log2(P)) + int(paired)  # slot rows from a layer's start to page p: p << shift
+    layer_elems = (2 if paired else 1) * s.pool_pages * P * H * D
+    cache_elems = s.num_layers * layer_elems  # of each cache, or of the one paired cache
+    v_offset = P * H * D if paired else 0  # v_cache - k_cache in elements within one paired buffer
     units = host_units(s, case.requests)
     tid = np.arange(WG)
     t0 = tid // cols
@@ -72,7 +75,15 @@ def emulate(case):
                 allowed[base + ko: base + ko + n * H * D * KBITS[t] // 8] = True
                 allowed[base + vo: base + vo + n * H * D * VBITS[t] // 8] = True
     per_unit = max(1, min(B, UNIT_ELEMS // (H * D)))
-    n_units = sum(-(-oracle.valid_tokens(r, B, b) // per_unit) for r in case.requests for b in oracle.reused_blocks(r))
+
+    def pieces(r, b):  # a block's rows cut at page boundaries and every per_unit tokens
+        t, n, count = 0, oracle.valid_tokens(r, B, b), 0
+        while t < n:
+            t += min(per_unit, P - (r.dst_row0 + b * B + t) % P, n - t)
+            count += 1
+        return count
+
+    n_units = sum(pieces(r, b) for r in case.requests for b in oracle.reused_blocks(r))
     assert len(units) == n_units * s.num_layers
     pt_all = np.concatenate([r.page_table for r in case.requests]).astype(np.int64)
     pt_start = np.cumsum([0] + [len(r.page_table) for r in case.requests])
@@ -88,10 +99,11 @@ def emulate(case):
         assert u["table_off"] == ri * D  # (cos, sin) table of this request, D doubles
         rows = u["row0"] + np.arange(n_valid)
         lp = rows >> int(np.log2(P))
+        assert (lp == lp[0]).all(), "a unit crosses a page boundary"
         assert (lp < len(r.page_table)).all()
         page = pt_all[u["pt_off"] + lp]
         assert ((page >= 0) & (page < s.pool_pages)).all()
-        dst_row = int(u["layer"]) * layer_elems + ((page << int(np.log2(P))) | (rows & (P - 1))) * H * D
+        dst_row = int(u["layer"]) * layer_elems + ((page << shift) | (rows & (P - 1))) * H * D
         kb, vb = KBITS[tag], VBITS[tag]
         if tag != 0:
             sc = int(u["scale_off"]) + 4 * head[active]
@@ -110,15 +122,25 @@ def emulate(case):
                 dst = dst_row[t] + head[sel] * D
                 for off in (8 * j[sel], D // 2 + 8 * j[sel]):
                     for d0 in dst + off:
-                        assert 0 <= d0 and d0 + 8 <= cache_elems
+                        assert 0 <= d0 and d0 + v_offset + 8 <= cache_elems
                         writes_k[d0: d0 + 8] += 1
-                        writes_v[d0: d0 + 8] += 1
+                        writes_v[d0 + v_offset: d0 + v_offset + 8] += 1
     assert not (payload_read & ~allowed).any(), "read outside the valid rows of reused blocks"
     assert (payload_read == allowed).all(), "some restored payload byte is never read"
-    written = oracle.written_slots(s, case.requests)
-    want = np.repeat(np.tile(written, s.num_layers), H * D).astype(np.int32)
-    assert np.array_equal(writes_k, want), "K writes differ from the restored rows"
-    assert np.array_equal(writes_v, want), "V writes differ from the restored rows"
+    written = oracle.written_slots(s, case.requests)  # [pool_slots], the same in every layer
+    if paired:  # [L][pool_pages][2][P][H*D]: K rows in half 0, V rows in half 1
+        rows_of = np.tile(written.reshape(s.pool_pages, 1, P), (s.num_layers, 1, 1))
+        want_k = np.zeros((s.num_layers * s.pool_pages, 2, P), np.int32)
+        want_v = np.zeros_like(want_k)
+        want_k[:, 0, :] = rows_of.reshape(-1, P)
+        want_v[:, 1, :] = rows_of.reshape(-1, P)
+        want_k = np.repeat(want_k.reshape(-1), H * D)
+        want_v = np.repeat(want_v.reshape(-1), H * D)
+        assert not (writes_k + writes_v > 1).any(), "a cache element written twice"
+    else:
+        want_k = want_v = np.repeat(np.tile(written, s.num_layers), H * D).astype(np.int32)
+    assert np.array_equal(writes_k, want_k), "K writes differ from the restored rows"
+    assert np.array_equal(writes_v, want_v), "V writes differ from the restored rows"
 
 
 @pytest.mark.parametrize("maker", [
@@ -136,4 +158,25 @@ def emulate(case):
                            tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2),
 ], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "d256_b64", "h32_b8", "h8_d128_split_units"])
 def test_kernel_addresses(maker):
+    emulate(maker())
+
+
+def _paired(case):
+    import dataclasses
+    case.shape = dataclasses.replace(case.shape, kv_layout=wl.KV_PAIRED)
+    return case
+
+
+@pytest.mark.parametrize("maker", [
+    lambda: _paired(wl.make_case("tiny")),
+    lambda: _paired(wl.make_custom(1, L=2, H=3, D=128, B=32, P=16, n_tokens=(70,), deltas=(12,), rho0s=(9,),
+                                   tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2)),
+    lambda: _paired(wl.make_custom(2, L=1, H=8, D=64, B=4, P=16, n_tokens=(23, 9), deltas=(5, 0), rho0s=(2, 40),
+                                   tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2)),
+    lambda: _paired(wl.make_custom(5, L=2, H=8, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,),
+                                   tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2)),
+    lambda: _paired(wl.make_custom(6, L=1, H=2, D=64, B=64, P=4, n_tokens=(130,), deltas=(1,), rho0s=(3,),
+                                   tag_set=(0, 2), mix=(1, 1), repair_frac=0.1)),
+], ids=["tiny", "h3_d128", "h8_b4_two_requests", "h8_d128_unaligned", "b64_p4"])
+def test_kernel_addresses_paired_pages(maker):
     emulate(maker())

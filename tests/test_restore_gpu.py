@@ -33,6 +33,49 @@ def test_named_small_full(name, torch):
     assert st.bit_exact_fraction > 0.9999
 
 
+def _paired(case):
+    import dataclasses
+    case.shape = dataclasses.replace(case.shape, kv_layout=wl.KV_PAIRED)
+    return case
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b_1l"])
+def test_named_small_full_paired_pages(name, torch):
+    log(f"[gpu] {name}, paired K/V pages: full-cache parity")
+    dr, ckpt = restore_small(_paired(wl.make_case(name)))
+    st = check_full(dr, ckpt)
+    log(f"  {st}")
+    assert st.bit_exact_fraction > 0.9999
+
+
+def test_paired_pages_argument_errors(torch):
+    """A paired cache is one buffer with v_cache = k_cache + P*H*D elements;
+    any other placement, or a buffer smaller than both halves of every
+    layer, is refused before any write."""
+    from paper_2609_26219_amd.device import DeviceRestore
+    case = _paired(wl.make_case("tiny"))
+    ckpt = oracle_checkpoint(case)
+    dr = DeviceRestore(case, checkpoint=ckpt)
+    s_ = case.shape
+    nb = lambda t: t.numel() * t.element_size()
+    half = s_.page_size * s_.row_elems * 2
+    p, sc, k = dr.payload, dr.scales, dr.k_cache
+    total = pb.cache_nbytes(dr.k_cache, dr.v_cache)
+    assert total == 2 * s_.cache_elems * 2
+    good = (p.data_ptr(), nb(p), sc.data_ptr(), nb(sc), k.data_ptr(), k.data_ptr() + half, total, 0)
+    assert pb.pkv_restore_status(dr.plan, *good) == pb.PKV_OK
+    torch.cuda.synchronize()
+    bad = [
+        good[:5] + (k.data_ptr() + half + 16,) + good[6:],   # V not right after the page's K slots
+        good[:5] + (k.data_ptr(),) + good[6:],               # V on top of K
+        good[:6] + (total // 2, 0),                          # one half's size
+        good[:4] + (p.data_ptr(), p.data_ptr() + half) + good[6:],  # cache over the payload
+    ]
+    for args in bad:
+        assert pb.pkv_restore_status(dr.plan, *args) == pb.PKV_ERR_INVALID_ARGUMENT, args
+    check_full(dr, ckpt)
+
+
 def test_tiny_k4v4_reading(torch):
     check_full(*restore_small(wl.make_case("tiny", int4_tag=wl.TAG_K4V4)))
 
@@ -50,12 +93,15 @@ PROPERTY_CASES = [
 ]
 
 
+@pytest.mark.parametrize("layout", [wl.KV_SEPARATE, wl.KV_PAIRED], ids=["separate", "paired"])
 @pytest.mark.parametrize("params", PROPERTY_CASES, ids=[f"case{i}" for i in range(len(PROPERTY_CASES))])
-def test_property_cases(params, torch):
+def test_property_cases(params, layout, torch):
     B, P, D, H, n, deltas, rho0s, tags, rep, out = params
     case = wl.make_custom(hash(params) & 0xFFFF, L=2, H=H, D=D, B=B, P=P, n_tokens=n, deltas=deltas, rho0s=rho0s,
                           tag_set=tags, mix=[1.0] * len(tags), repair_frac=rep, out_dtype=out, outlier_pairs=1)
-    log(f"[gpu] property case {params}")
+    if layout == wl.KV_PAIRED:
+        _paired(case)
+    log(f"[gpu] property case {params} layout {layout}")
     check_full(*restore_small(case))
 
 
@@ -190,6 +236,12 @@ def _full_size(case, samples, torch):
 def test_llama8b_32l_full_size(torch):
     log("[gpu] llama8b_32l: full-size checkpoint + restore, 3 sampled layers + untouched check")
     st = _full_size(wl.make_case("llama8b_32l"), [(0, 0), (0, 17), (0, 31)], torch)
+    log(f"  {st}")
+
+
+def test_llama8b_32l_full_size_paired_pages(torch):
+    log("[gpu] llama8b_32l, paired K/V pages: full-size checkpoint + restore, 2 sampled layers + untouched check")
+    st = _full_size(_paired(wl.make_case("llama8b_32l")), [(0, 3), (0, 30)], torch)
     log(f"  {st}")
 
 

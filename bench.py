@@ -18,6 +18,7 @@ workload, is reported beside it as ``cpu_baseline``.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import multiprocessing as mp
@@ -47,6 +48,12 @@ WORKLOAD_TEXT = {
 }
 
 
+KV_LAYOUT_TEXT = {
+    "paired": "paired: one cache [L][pool_pages][2][P][H][D], a page's K slots then its V slots",
+    "separate": "separate: k_cache and v_cache, each [L][pool_pages][P][H][D]",
+}
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -55,10 +62,10 @@ def kernel_hash(src: str = KERNEL_SRC) -> str:
     return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str, int4: str, kernel: str = "restore_kernel", src: str = KERNEL_SRC):
+def measured_traffic(workload: str, int4: str, layout: str, kernel: str = "restore_kernel", src: str = KERNEL_SRC):
     """HBM bytes per launch from the committed rocprofv3 PMC summary, if it was
     taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_{int4.lower()}_pmc.md")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_{int4.lower()}_{layout}_pmc.md")
     if not os.path.exists(path):
         return None
     m = re.search(r"^traffic-json: (\{.*\})\s*$", open(path).read(), re.M)
@@ -346,6 +353,32 @@ def representations(torch, binding, wl, case, old, steps: int, host_steps: int, 
     return rows
 
 
+def other_layout(torch, wl, case, dr, stream, steps: int = 20):
+    """The same restore (same checkpoint, plan inputs and page tables) into
+    caches of the other layout, for comparison."""
+    from paper_2609_26219_amd.device import DeviceRestore
+
+    other = wl.KV_SEPARATE if case.shape.kv_layout == wl.KV_PAIRED else wl.KV_PAIRED
+    c = wl.Case(case.name, dataclasses.replace(case.shape, kv_layout=other), case.requests, case.seed,
+                case.distinct_layers, case.outlier_pairs)
+    d2 = DeviceRestore(c, checkpoint=(dr.payload, dr.scales))
+    info = d2.info
+    nbytes = info["bytes_read"] + info["bytes_written"]
+    ms, _ = time_launches(torch, lambda i: d2.run(stream), steps, 3, stream)
+    avg = sum(ms) / len(ms)
+    del d2
+    torch.cuda.empty_cache()
+    name = "paired" if other == wl.KV_PAIRED else "separate"
+    log(f"[bench] {name} caches: {avg * 1e3:.1f} us ({100 * nbytes / (avg * 1e-3) / 1e9 / HBM_PEAK_GBPS:.2f}% HBM)")
+    return {
+        "kv_layout": KV_LAYOUT_TEXT[name],
+        "us_per_restore": round(avg * 1e3, 1),
+        "us_p10_p50_p90": [round(ms[int(q * (len(ms) - 1))] * 1e3, 1) for q in (0.1, 0.5, 0.9)],
+        "GBps": round(nbytes / (avg * 1e-3) / 1e9, 1),
+        "pct_hbm_peak": round(100 * nbytes / (avg * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+    }
+
+
 def copy_reference(torch, nbytes: int = 4 << 30, reps: int = 10):
     """Plain device-to-device copy (read + write bytes / time): the practical ceiling."""
     src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -372,6 +405,8 @@ def main():
     ap.add_argument("--workload", default="llama8b_32l", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--int4", default="K8V4", choices=["K8V4", "K4V4"],
                     help="representation of the int4 tag: K8V4 (the paper's tier) or uniform K4V4")
+    ap.add_argument("--kv-layout", default="paired", choices=["paired", "separate"],
+                    help="paged cache layout: one [L][pool_pages][2][P][H][D] cache (paired) or two caches")
     ap.add_argument("--sets", type=int, default=2, help="buffer sets cycled between steps")
     ap.add_argument("--write-steps", type=int, default=10, help="timed checkpoint-write launches")
     ap.add_argument("--host-steps", type=int, default=10, help="timed streamed restores from pinned host memory")
@@ -379,6 +414,7 @@ def main():
                     help="skip the uniform-representation comparison (FP16 / K8V8 / K8V4 / K4V4 / mixed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ref", action="store_true")
+    ap.add_argument("--no-other-layout", action="store_true", help="skip timing the restore on the other cache layout")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -399,6 +435,8 @@ def main():
     int4_tag = wl.TAG_K8V4 if args.int4 == "K8V4" else wl.TAG_K4V4
     t = time.perf_counter()
     case = wl.make_case(args.workload, int4_tag=int4_tag)
+    layout = wl.KV_PAIRED if args.kv_layout == "paired" else wl.KV_SEPARATE
+    case.shape = dataclasses.replace(case.shape, kv_layout=layout)
     old = OldCaches(case)
     log(f"[bench] drew {args.workload} old caches in {time.perf_counter() - t:.1f} s")
     stream = torch.cuda.current_stream()
@@ -453,6 +491,7 @@ def main():
             "bytes_read": info["bytes_read"],
             "bytes_written": info["bytes_written"],
             "buffer_sets": len(sets),
+            "kv_layout": KV_LAYOUT_TEXT[args.kv_layout],
         },
         "us_per_restore": round(kern_avg_ms * 1e3, 1),
         "us_per_restore_p10_p50_p90": [round(kern_ms[int(q * (len(kern_ms) - 1))] * 1e3, 1) for q in (0.1, 0.5, 0.9)],
@@ -465,7 +504,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": measured_traffic(args.workload, args.int4),
+            "traffic": measured_traffic(args.workload, args.int4, args.kv_layout),
         },
         "checkpoint_write": {
             "what": "pkv_quantize_gather of every block of every layer from the old paged caches "
@@ -482,10 +521,13 @@ def main():
                 "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s",
                 "frac": round(w_achieved / HBM_PEAK_GBPS, 4),
-                "traffic": measured_traffic(args.workload, args.int4, "gather_tile_kernel", GATHER_SRC),
+                "traffic": measured_traffic(args.workload, args.int4, args.kv_layout, "gather_tile_kernel",
+                                            GATHER_SRC),
             },
         },
     }
+    if not args.no_other_layout:
+        out["other_kv_layout"] = other_layout(torch, wl, case, sets[0], stream)
     if args.host_steps > 0:
         out["host_restore"] = host_restore(torch, binding, sets[0], args.host_steps, stream)
     if not args.no_representations:

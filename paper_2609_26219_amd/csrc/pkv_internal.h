@@ -11,6 +11,11 @@
 namespace pkv {
 
 constexpr int kMaxHeadDim = 512;
+// Restore workgroups resident per compute unit (one wave per SIMD each).
+// Three measured fastest: 913 vs 953 us on the 8B-shaped 32-layer restore
+// with paired pages, 1000 vs 1027 us with separate caches, 4849 vs 4965 us
+// on the 70B shape; two was no faster than four, the register limit.
+constexpr int kRestoreWorkgroupsPerCU = 3;
 constexpr int kMaxRowElems = 4096;   // num_kv_heads * head_dim
 constexpr int kMaxBlockTokens = 1024;
 constexpr int kWorkgroup = 256;       // threads per workgroup
@@ -125,6 +130,9 @@ struct pkv_plan {
   double* d_tables = nullptr;
   int32_t* d_page_tables = nullptr;
   int device = -1;
+  // Dynamic LDS bytes per restore workgroup, sized so that at most
+  // kRestoreWorkgroupsPerCU workgroups are resident on a compute unit.
+  uint32_t restore_lds = 0;
   // Streamed restore: copy streams and events (hipStream_t / hipEvent_t),
   // created on first use.  events[0] marks the caller's stream at entry;
   // events[1 + l * n + k] the end of layer l's chunks on copy stream k.

@@ -3,18 +3,25 @@
 // and the C entry points that own device memory and launch it.
 //
 // Work decomposition.  One workgroup restores one unit: every head of up to
-// 16K output elements' worth of consecutive tokens (16 tokens at 8 heads x
-// 128) of one reused block of one layer.  The unit's K rows and V rows are
-// contiguous in the payload (token-major tiles) and each token lands on one
-// cache slot whose H*D elements are contiguous, so a unit is a streaming
+// 16K output elements' worth of consecutive tokens of one reused block of
+// one layer that share one cache page (at 8 heads x 128 and 16-token pages,
+// the block's rows in each page it touches).  The unit's K rows and V rows
+// are contiguous in the payload (token-major tiles) and each token lands on
+// one cache slot whose H*D elements are contiguous, so a unit is a streaming
 // row-to-row transform.  A thread owns a fixed piece of every row it
 // touches: channels [8j, 8j+8) and [D/2+8j, D/2+8j+8) of one head.  For keys
 // that is a set of whole rotary pairs, so the rotation needs no cross-lane
 // exchange; for keys and values alike, each store instruction of a wave
-// writes whole 128-byte lines.  Threads (t0, c), c = head*(D/16) + j, walk
-// tokens t0, t0+tpp, ... with tpp = 256 / (H*D/16); each looks up its
-// token's page itself, so no workgroup-wide staging or barrier is needed
-// except for the per-request cos/sin table.
+// writes whole 128-byte lines.  Threads (t0, c), c = head*(D/16) + j, own
+// tokens t0, t0+tpp, ... with tpp = 256 / (H*D/16) (at most four of them)
+// and issue the loads of all their tokens before the first store; each
+// looks up its token's page itself, so no workgroup-wide staging or barrier
+// is needed except for the per-request cos/sin table.  At most three
+// workgroups share a compute unit (an LDS claim enforces it).
+//
+// Cache layouts.  With separate caches a page's K slots and V slots sit in
+// two buffers; with paired pages they are one contiguous run, K then V.
+// Both are addressed as page << page_shift slot rows from the layer's start.
 //
 // Arithmetic.  Codes decode exactly.  Keys are rotated in double precision
 // (full rate on CDNA4) with a double (cos, sin) table, so the rotated value
@@ -23,11 +30,13 @@
 // the hardware round-to-nearest-even conversions.
 //
 // Memory behaviour (8B-shaped 32K-token workload, measured): the kernel
-// moves 1.003x the algorithmic bytes; the write-heavy mixed stream bounds it.
+// moves 1.004x the algorithmic bytes; the write-heavy mixed stream bounds it,
+// and paired pages let the memory system stream the writes faster.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 
 #include "pkv.h"
@@ -36,8 +45,9 @@
 namespace pkv {
 namespace {
 
-// Four waves per SIMD: measured as fast as eight for this kernel, and it lets
-// the (cos, sin) pairs of a thread stay in registers.
+// Register budget for four waves per SIMD, so that the (cos, sin) pairs and
+// four tokens' payload of a thread stay in registers (the residency cap of
+// three workgroups per compute unit then keeps three).
 constexpr int kMinWavesPerEU = 4;
 
 struct KernelArgs {
@@ -407,6 +417,19 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   }
   plan->device = dev;
   plan->host.info.device = dev;
+  // Residency cap through LDS: each restore workgroup claims a share of the
+  // compute unit's LDS (it needs only its table) so that no more than
+  // kRestoreWorkgroupsPerCU fit.
+  int lds_cu = 0, lds_wg = 0;
+  if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
+      hipDeviceGetAttribute(&lds_wg, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && lds_cu > 0) {
+    const int64_t table = int64_t(kMaxHeadDim) * int64_t(sizeof(double));
+    const int64_t share = (int64_t(lds_cu) / kRestoreWorkgroupsPerCU + int64_t(lds_cu) / (kRestoreWorkgroupsPerCU + 1)) / 2;
+    const int64_t dyn = std::min<int64_t>((share - table) & ~int64_t(255), int64_t(lds_wg) - table);
+    plan->restore_lds = dyn > 0 ? uint32_t(dyn) : 0;
+  } else {
+    (void)hipGetLastError();
+  }
   if (total > 0) {
     hipError_t e = hipMalloc(&plan->device_mem, total);
     if (e != hipSuccess) {
@@ -515,13 +538,13 @@ pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const voi
   const dim3 grid(static_cast<uint32_t>(n)), block(kWorkgroup);
   const bool bf16 = m.out_dtype == PKV_OUT_BF16, half = m.rope_style == PKV_ROPE_HALF;
   if (bf16 && half)
-    hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_HALF>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_HALF>), grid, block, plan->restore_lds, stream, a);
   else if (bf16)
-    hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_INTERLEAVED>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_INTERLEAVED>), grid, block, plan->restore_lds, stream, a);
   else if (half)
-    hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_HALF>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_HALF>), grid, block, plan->restore_lds, stream, a);
   else
-    hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_INTERLEAVED>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_INTERLEAVED>), grid, block, plan->restore_lds, stream, a);
   return hipGetLastError() == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
 }
 

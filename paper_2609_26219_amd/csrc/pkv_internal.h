@@ -11,11 +11,16 @@
 namespace pkv {
 
 constexpr int kMaxHeadDim = 512;
-// Restore workgroups resident per compute unit (one wave per SIMD each).
-// Three measured fastest: 913 vs 953 us on the 8B-shaped 32-layer restore
-// with paired pages, 1000 vs 1027 us with separate caches, 4849 vs 4965 us
-// on the 70B shape; two was no faster than four, the register limit.
-constexpr int kRestoreWorkgroupsPerCU = 3;
+// Restore workgroups resident per compute unit (one wave per SIMD each; four
+// is the register limit), chosen per plan from its read:write byte ratio.
+// Measured on the 8B-shaped 32-layer restore, paired pages, us for 2/3/4:
+//   FP16 (ratio 1.00)  1227-1235 / 1277 / 1282-1290
+//   K8V8 (0.50)         922-942 /  891 /  929-942
+//   mixed (0.47)        936-978 /  908 /  952
+//   K8V4 (0.38)         892-931 /  870 /  886-889
+//   K4V4 (0.25)         931-963 /  830 /  808
+// and with separate caches 1000 vs 1027 us (3 vs 4) on the mixed tags.
+int restore_workgroups_per_cu(uint64_t bytes_read, uint64_t bytes_written);
 constexpr int kMaxRowElems = 4096;   // num_kv_heads * head_dim
 constexpr int kMaxBlockTokens = 1024;
 constexpr int kWorkgroup = 256;       // threads per workgroup
@@ -131,7 +136,7 @@ struct pkv_plan {
   int32_t* d_page_tables = nullptr;
   int device = -1;
   // Dynamic LDS bytes per restore workgroup, sized so that at most
-  // kRestoreWorkgroupsPerCU workgroups are resident on a compute unit.
+  // restore_workgroups_per_cu() workgroups are resident on a compute unit.
   uint32_t restore_lds = 0;
   // Streamed restore: copy streams and events (hipStream_t / hipEvent_t),
   // created on first use.  events[0] marks the caller's stream at entry;

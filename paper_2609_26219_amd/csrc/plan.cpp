@@ -125,6 +125,14 @@ bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache
   return true;
 }
 
+int restore_workgroups_per_cu(uint64_t bytes_read, uint64_t bytes_written) {
+  // Units that read more per byte written hold more bytes in flight each, so
+  // fewer of them keep the memory system busy.
+  if (bytes_written == 0) return 4;
+  const double ratio = double(bytes_read) / double(bytes_written);
+  return ratio >= 0.75 ? 2 : ratio >= 0.3 ? 3 : 4;
+}
+
 int32_t unit_tokens(const pkv_model_t& m) {
   const int64_t per = kUnitElems / (int64_t(m.num_kv_heads) * m.head_dim);
   return int32_t(std::max<int64_t>(1, std::min<int64_t>(per, m.block_tokens)));

@@ -16,8 +16,9 @@
 // tokens t0, t0+tpp, ... with tpp = 256 / (H*D/16) (at most four of them)
 // and issue the loads of all their tokens before the first store; each
 // looks up its token's page itself, so no workgroup-wide staging or barrier
-// is needed except for the per-request cos/sin table.  At most three
-// workgroups share a compute unit (an LDS claim enforces it).
+// is needed except for the per-request cos/sin table.  An LDS claim caps
+// the workgroups sharing a compute unit at two to four, chosen per plan from
+// its read:write byte ratio.
 //
 // Cache layouts.  With separate caches a page's K slots and V slots sit in
 // two buffers; with paired pages they are one contiguous run, K then V.
@@ -46,8 +47,8 @@ namespace pkv {
 namespace {
 
 // Register budget for four waves per SIMD, so that the (cos, sin) pairs and
-// four tokens' payload of a thread stay in registers (the residency cap of
-// three workgroups per compute unit then keeps three).
+// four tokens' payload of a thread stay in registers (the residency cap then
+// keeps two to four).
 constexpr int kMinWavesPerEU = 4;
 
 struct KernelArgs {
@@ -419,14 +420,15 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   plan->host.info.device = dev;
   // Residency cap through LDS: each restore workgroup claims a share of the
   // compute unit's LDS (it needs only its table) so that no more than
-  // kRestoreWorkgroupsPerCU fit.
+  // restore_workgroups_per_cu() fit.
   int lds_cu = 0, lds_wg = 0;
   if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
       hipDeviceGetAttribute(&lds_wg, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && lds_cu > 0) {
     const int64_t table = int64_t(kMaxHeadDim) * int64_t(sizeof(double));
-    const int64_t share = (int64_t(lds_cu) / kRestoreWorkgroupsPerCU + int64_t(lds_cu) / (kRestoreWorkgroupsPerCU + 1)) / 2;
+    const int64_t n = restore_workgroups_per_cu(plan->host.info.bytes_read, plan->host.info.bytes_written);
+    const int64_t share = (int64_t(lds_cu) / n + int64_t(lds_cu) / (n + 1)) / 2;
     const int64_t dyn = std::min<int64_t>((share - table) & ~int64_t(255), int64_t(lds_wg) - table);
-    plan->restore_lds = dyn > 0 ? uint32_t(dyn) : 0;
+    plan->restore_lds = n < 4 && dyn > 0 ? uint32_t(dyn) : 0;
   } else {
     (void)hipGetLastError();
   }

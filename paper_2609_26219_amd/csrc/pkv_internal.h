@@ -48,8 +48,8 @@ struct Unit {
   int32_t layer;
   int32_t tag;         // bits 0-7: pkv_tag_t; bit 8: rotate keys (Delta != 0)
   int32_t n_valid;     // tokens in the unit
-  int32_t page1;       // checkpoint: the next two physical pages of the block's rows,
-  int32_t page2;       //   -1 past its last page; restore: 0
+  int32_t page1;       // checkpoint: the next two physical pages of the block's rows, -1 past its
+  int32_t page2;       //   last page; restore: page1 = the one physical page of the unit's rows, page2 = 0
 };
 static_assert(sizeof(Unit) == 64, "Unit layout");
 constexpr int32_t kUnitRotate = 1 << 8;

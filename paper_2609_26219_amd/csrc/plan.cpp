@@ -295,7 +295,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
             u.layer = int32_t(l);
             u.tag = tag | (q.delta != 0 ? kUnitRotate : 0);
             u.n_valid = int32_t(len);
-            u.page1 = 0;
+            u.page1 = q.page_table[(q.dst_row0 + b * B + t0) >> lp2];  // validated above; one page per unit
             u.page2 = 0;
             hp.units.push_back(u);
           }

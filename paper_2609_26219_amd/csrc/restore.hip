@@ -14,9 +14,9 @@
 // exchange; for keys and values alike, each store instruction of a wave
 // writes whole 128-byte lines.  Threads (t0, c), c = head*(D/16) + j, own
 // tokens t0, t0+tpp, ... with tpp = 256 / (H*D/16) (at most four of them)
-// and issue the loads of all their tokens before the first store; each
-// looks up its token's page itself, so no workgroup-wide staging or barrier
-// is needed except for the per-request cos/sin table.  An LDS claim caps
+// and issue the loads of all their tokens before the first store; the
+// unit's one page comes with its work item, so no workgroup-wide staging or
+// barrier is needed except for the per-request cos/sin table.  An LDS claim caps
 // the workgroups sharing a compute unit at two to four, chosen per plan from
 // its read:write byte ratio.
 //
@@ -54,7 +54,6 @@ constexpr int kMinWavesPerEU = 4;
 struct KernelArgs {
   const Unit* units;
   const double* tables;
-  const int32_t* page_tables;
   const uint8_t* payload;
   const uint16_t* scales;
   uint16_t* k_cache;
@@ -278,11 +277,12 @@ struct Piece {
   int head, j;
   KeyPiece kp;
   float ks, kz, vs, vz;
-  int64_t lbase;  // cache element offset of the unit's layer and the thread's head
+  int64_t pbase;  // cache element offset of the unit's page, in its layer, at the thread's head
 };
 
 // NK tokens of one thread (t, t + tpp, ...): every load is issued before the
-// first store, so a wave keeps NK tokens of payload in flight.
+// first store, so a wave keeps NK tokens of payload in flight.  No load
+// depends on another: the unit's page comes with its work item.
 template <int NK, int TAG, bool ROT, int STYLE, bool BF16>
 __device__ __forceinline__ void restore_tokens(const KernelArgs& a, const Unit& u, int t, const Piece& q,
                                                const double2* __restrict__ cs) {
@@ -300,8 +300,7 @@ __device__ __forceinline__ void restore_tokens(const KernelArgs& a, const Unit& 
   for (int k = 0; k < NK; ++k) {
     const int tk = t + k * a.tpp;
     const int64_t row = u.row0 + tk;
-    const int64_t page = a.page_tables[u.pt_off + (row >> a.log2P)];
-    dst[k] = q.lbase + ((page << a.page_shift) | (row & slot_mask)) * row_elems;
+    dst[k] = q.pbase + (row & slot_mask) * row_elems;
     const int64_t r = int64_t(tk) * H + q.head;
     klo[k].load(kbase + r * (D * KB / 8) + q.kp.lo * KB / 8);
     khi[k].load(kbase + r * (D * KB / 8) + q.kp.hi * KB / 8);
@@ -330,7 +329,9 @@ __device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u,
     q.vs = half_bits_to_float(sw.y & 0xFFFFu);
     q.vz = half_bits_to_float(sw.y >> 16);
   }
-  q.lbase = int64_t(u.layer) * a.layer_elems + int64_t(head) * a.D;
+  // A unit's rows share one page, carried in its work item.
+  q.pbase = int64_t(u.layer) * a.layer_elems + (int64_t(u.page1) << a.page_shift) * (int64_t(a.H) * a.D) +
+            int64_t(head) * a.D;
   double2 cs[8];  // (cos, sin) of this thread's eight rotary pairs
   if constexpr (ROT) {
 #pragma unroll
@@ -409,7 +410,8 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t n_units = plan->host.units.size() * sizeof(Unit);
   const size_t n_tab = plan->host.tables.size() * sizeof(double);
-  const size_t n_pt = plan->host.page_tables.size() * sizeof(int32_t);
+  // Restore work items carry their page; only checkpoint plans read page tables on the device.
+  const size_t n_pt = plan->host.kind == 1 ? plan->host.page_tables.size() * sizeof(int32_t) : 0;
   const size_t total = al(n_units) + al(n_tab) + al(n_pt);
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) {
@@ -524,7 +526,6 @@ pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const voi
   KernelArgs a;
   a.units = plan->d_units + u0;
   a.tables = plan->d_tables;
-  a.page_tables = plan->d_page_tables;
   a.payload = static_cast<const uint8_t*>(payload);
   a.scales = static_cast<const uint16_t*>(scales);
   a.k_cache = static_cast<uint16_t*>(k_cache);

@@ -4,8 +4,9 @@ Takes the work list the host plan builds (through an internal test hook of
 libpkv), replays the thread -> (token, head, piece) mapping and the address
 formulas of ``restore.hip`` for every thread of every workgroup, and checks:
 every read stays inside the payload/scales and inside the valid rows of a
-reused block's tiles; every write stays inside the caches; every element of
-every restored row is written exactly once and nothing else is written.
+reused block's tiles; each work item carries the one page its rows map to;
+every write stays inside the caches; every element of every restored row is
+written exactly once and nothing else is written.
 Keep the constants below in step with the kernel's launch code.
 """
 import ctypes
@@ -103,6 +104,8 @@ def emulate(case):
         assert (lp < len(r.page_table)).all()
         page = pt_all[u["pt_off"] + lp]
         assert ((page >= 0) & (page < s.pool_pages)).all()
+        assert (page == u["page1"]).all(), "the work item's page is not the rows' page"
+        page = np.full(n_valid, int(u["page1"]), dtype=np.int64)  # what the kernel uses
         dst_row = int(u["layer"]) * layer_elems + ((page << shift) | (rows & (P - 1))) * H * D
         kb, vb = KBITS[tag], VBITS[tag]
         if tag != 0:

@@ -12,15 +12,17 @@ namespace pkv {
 
 constexpr int kMaxHeadDim = 512;
 // Restore workgroups resident per compute unit (one wave per SIMD each; four
-// is the register limit), chosen per plan from its read:write byte ratio.
-// Measured on the 8B-shaped 32-layer restore, paired pages, us for 2/3/4:
-//   FP16 (ratio 1.00)  1227-1235 / 1277 / 1282-1290
-//   K8V8 (0.50)         922-942 /  891 /  929-942
-//   mixed (0.47)        936-978 /  908 /  952
-//   K8V4 (0.38)         892-931 /  870 /  886-889
-//   K4V4 (0.25)         931-963 /  830 /  808
-// and with separate caches 1000 vs 1027 us (3 vs 4) on the mixed tags.
-int restore_workgroups_per_cu(uint64_t bytes_read, uint64_t bytes_written);
+// is the register limit), chosen per plan.  Measured on the 8B-shaped
+// 32-layer restore, paired pages, destination rows 7 slots into a page
+// (units of 9, 16 and 7 tokens), us for 2/3/4:
+//   FP16 (read:write 1.00)  1227-1235 / 1277 / 1282-1290
+//   K8V8 (0.50)              922-942 /  891 /  929-942
+//   mixed (0.47)             936-978 /  908 /  952
+//   K8V4 (0.38)              892-931 /  870 /  886-889
+//   K4V4 (0.25)              931-963 /  830 /  808
+// and with page-aligned rows (16-token units) 910 / 955 / 958 for the mixed
+// tags: the best count falls as units grow.
+int restore_workgroups_per_cu(const pkv_plan_info_t& info, const pkv_model_t& m);
 constexpr int kMaxRowElems = 4096;   // num_kv_heads * head_dim
 constexpr int kMaxBlockTokens = 1024;
 constexpr int kWorkgroup = 256;       // threads per workgroup

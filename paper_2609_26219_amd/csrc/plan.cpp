@@ -125,12 +125,16 @@ bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache
   return true;
 }
 
-int restore_workgroups_per_cu(uint64_t bytes_read, uint64_t bytes_written) {
-  // Units that read more per byte written hold more bytes in flight each, so
-  // fewer of them keep the memory system busy.
-  if (bytes_written == 0) return 4;
-  const double ratio = double(bytes_read) / double(bytes_written);
-  return ratio >= 0.75 ? 2 : ratio >= 0.3 ? 3 : 4;
+int restore_workgroups_per_cu(const pkv_plan_info_t& info, const pkv_model_t& m) {
+  // The memory system streams best with about 32K output elements of work in
+  // flight per compute unit (two thirds of that for read-heavy plans, four
+  // thirds for write-heavy ones): so many units at a time, two to four.
+  if (info.num_units == 0 || info.bytes_written == 0) return 4;
+  const double ratio = double(info.bytes_read) / double(info.bytes_written);
+  const double target = 32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 4.0 / 3.0);
+  const double unit_elems = double(info.restored_rows) * m.num_kv_heads * m.head_dim / double(info.num_units);
+  const double n = std::floor(target / unit_elems + 0.5);
+  return n < 2 ? 2 : n > 4 ? 4 : int(n);
 }
 
 int32_t unit_tokens(const pkv_model_t& m) {
@@ -281,9 +285,10 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
           const int64_t n_valid = std::min<int64_t>(B, q.suffix_tokens - b * B);
           // Split the block into units of at most `per_unit` tokens that
           // never cross a page boundary, so a unit writes slots of one page.
+          // A page's run of rows is cut into equal parts (17 -> 9 + 8, not 16 + 1).
           for (int64_t t0 = 0, len = 0; t0 < n_valid; t0 += len) {
-            const int64_t to_page_end = P - ((q.dst_row0 + b * B + t0) & (P - 1));
-            len = std::min<int64_t>(std::min<int64_t>(per_unit, to_page_end), n_valid - t0);
+            const int64_t run = std::min<int64_t>(P - ((q.dst_row0 + b * B + t0) & (P - 1)), n_valid - t0);
+            len = ceil_div(run, ceil_div(run, per_unit));
             Unit u;
             const uint64_t block_base = layer_base + block_off[r][b];
             u.k_off = block_base + uint64_t(t0) * H * D * kKeyBits[tag] / 8;

@@ -77,11 +77,12 @@ def emulate(case):
                 allowed[base + vo: base + vo + n * H * D * VBITS[t] // 8] = True
     per_unit = max(1, min(B, UNIT_ELEMS // (H * D)))
 
-    def pieces(r, b):  # a block's rows cut at page boundaries and every per_unit tokens
+    def pieces(r, b):  # a block's rows cut at page boundaries, each page's run into ceil(run / per_unit) parts
         t, n, count = 0, oracle.valid_tokens(r, B, b), 0
         while t < n:
-            t += min(per_unit, P - (r.dst_row0 + b * B + t) % P, n - t)
-            count += 1
+            run = min(P - (r.dst_row0 + b * B + t) % P, n - t)
+            count += -(-run // per_unit)
+            t += run
         return count
 
     n_units = sum(pieces(r, b) for r in case.requests for b in oracle.reused_blocks(r))

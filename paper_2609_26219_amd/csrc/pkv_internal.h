@@ -20,8 +20,9 @@ constexpr int kMaxHeadDim = 512;
 //   mixed (0.47)             936-978 /  908 /  952
 //   K8V4 (0.38)              892-931 /  870 /  886-889
 //   K4V4 (0.25)              931-963 /  830 /  808
-// and with page-aligned rows (16-token units) 910 / 955 / 958 for the mixed
-// tags: the best count falls as units grow.
+// and with page-aligned rows (16-token units) 902-921 / 960-966 / 958 for
+// the mixed tags, 765-771 / 827-838 / 838-846 for K4V4: the best count falls
+// as units grow.
 int restore_workgroups_per_cu(const pkv_plan_info_t& info, const pkv_model_t& m);
 constexpr int kMaxRowElems = 4096;   // num_kv_heads * head_dim
 constexpr int kMaxBlockTokens = 1024;

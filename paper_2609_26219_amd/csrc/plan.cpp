@@ -127,11 +127,11 @@ bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache
 
 int restore_workgroups_per_cu(const pkv_plan_info_t& info, const pkv_model_t& m) {
   // The memory system streams best with about 32K output elements of work in
-  // flight per compute unit (two thirds of that for read-heavy plans, four
-  // thirds for write-heavy ones): so many units at a time, two to four.
+  // flight per compute unit (two thirds of that for read-heavy plans, six
+  // fifths for write-heavy ones): so many units at a time, two to four.
   if (info.num_units == 0 || info.bytes_written == 0) return 4;
   const double ratio = double(info.bytes_read) / double(info.bytes_written);
-  const double target = 32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 4.0 / 3.0);
+  const double target = 32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 1.2);
   const double unit_elems = double(info.restored_rows) * m.num_kv_heads * m.head_dim / double(info.num_units);
   const double n = std::floor(target / unit_elems + 0.5);
   return n < 2 ? 2 : n > 4 ? 4 : int(n);

@@ -11,19 +11,6 @@
 namespace pkv {
 
 constexpr int kMaxHeadDim = 512;
-// Restore workgroups resident per compute unit (one wave per SIMD each; four
-// is the register limit), chosen per plan.  Measured on the 8B-shaped
-// 32-layer restore, paired pages, destination rows 7 slots into a page
-// (units of 9, 16 and 7 tokens), us for 2/3/4:
-//   FP16 (read:write 1.00)  1227-1235 / 1277 / 1282-1290
-//   K8V8 (0.50)              922-942 /  891 /  929-942
-//   mixed (0.47)             936-978 /  908 /  952
-//   K8V4 (0.38)              892-931 /  870 /  886-889
-//   K4V4 (0.25)              931-963 /  830 /  808
-// and with page-aligned rows (16-token units) 902-921 / 960-966 / 958 for
-// the mixed tags, 765-771 / 827-838 / 838-846 for K4V4: the best count falls
-// as units grow.
-int restore_workgroups_per_cu(const pkv_plan_info_t& info, const pkv_model_t& m);
 constexpr int kMaxRowElems = 4096;   // num_kv_heads * head_dim
 constexpr int kMaxBlockTokens = 1024;
 constexpr int kWorkgroup = 256;       // threads per workgroup
@@ -109,7 +96,24 @@ struct HostPlan {
   std::vector<int64_t> layer_units;
   std::vector<CopyRange> payload_ranges, scale_ranges;
   std::vector<int64_t> payload_layer, scale_layer;
+  int64_t rotated_rows = 0;  // restore plans: restored rows whose keys rotate (shift != 0)
 };
+
+// Restore workgroups resident per compute unit (one wave per SIMD each; four
+// is the register limit), chosen per plan.  Measured on the 8B-shaped
+// 32-layer restore, paired pages, destination rows 7 slots into a page
+// (units of 9, 16 and 7 tokens), us for 2/3/4:
+//   FP16 (read:write 1.00)  1227-1235 / 1277 / 1282-1290
+//   K8V8 (0.50)              922-942 /  891 /  929-942
+//   mixed (0.47)             936-978 /  908 /  952
+//   K8V4 (0.38)              892-931 /  870 /  886-889
+//   K4V4 (0.25)              931-963 /  830 /  808
+// and with page-aligned rows (16-token units) 902-921 / 960-966 / 958 for
+// the mixed tags, 765-771 / 827-838 / 838-846 for K4V4: the best count falls
+// as units grow.  With no shift (no rotation, no table) the same unaligned
+// plans run best with fewer: mixed 900 / 961 / 978, K8V8 876 / 958 / 967,
+// K8V4 835-839 / 914-918 / 925, K4V4 820 / 802 / 836-842.
+int restore_workgroups_per_cu(const HostPlan& hp);
 
 // Validate and build the host side of a plan.  Makes no HIP call.
 pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,

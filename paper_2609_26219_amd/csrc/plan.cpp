@@ -125,14 +125,19 @@ bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache
   return true;
 }
 
-int restore_workgroups_per_cu(const pkv_plan_info_t& info, const pkv_model_t& m) {
+int restore_workgroups_per_cu(const HostPlan& hp) {
   // The memory system streams best with about 32K output elements of work in
   // flight per compute unit (two thirds of that for read-heavy plans, six
-  // fifths for write-heavy ones): so many units at a time, two to four.
-  if (info.num_units == 0 || info.bytes_written == 0) return 4;
+  // fifths for write-heavy ones, three quarters for units that do not rotate
+  // their keys): so many units at a time, two to four.
+  const pkv_plan_info_t& info = hp.info;
+  if (info.num_units == 0 || info.bytes_written == 0 || info.restored_rows == 0) return 4;
   const double ratio = double(info.bytes_read) / double(info.bytes_written);
-  const double target = 32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 1.2);
-  const double unit_elems = double(info.restored_rows) * m.num_kv_heads * m.head_dim / double(info.num_units);
+  const double rotated = double(hp.rotated_rows) / double(info.restored_rows);
+  const double target =
+      32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 1.2) * (0.75 + 0.25 * rotated);
+  const double unit_elems =
+      double(info.restored_rows) * hp.model.num_kv_heads * hp.model.head_dim / double(info.num_units);
   const double n = std::floor(target / unit_elems + 0.5);
   return n < 2 ? 2 : n > 4 ? 4 : int(n);
 }
@@ -305,6 +310,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
             hp.units.push_back(u);
           }
           hp.info.restored_rows += n_valid;
+          if (q.delta != 0) hp.rotated_rows += n_valid;
           hp.info.bytes_read += uint64_t(n_valid) * H * D * (kKeyBits[tag] + kValueBits[tag]) / 8;
           if (tag != PKV_TAG_FP16) hp.info.bytes_read += uint64_t(H) * 4 * 2;
         }

@@ -427,7 +427,7 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
       hipDeviceGetAttribute(&lds_wg, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && lds_cu > 0) {
     const int64_t table = int64_t(kMaxHeadDim) * int64_t(sizeof(double));
-    const int64_t n = restore_workgroups_per_cu(plan->host.info, plan->host.model);
+    const int64_t n = restore_workgroups_per_cu(plan->host);
     const int64_t share = (int64_t(lds_cu) / n + int64_t(lds_cu) / (n + 1)) / 2;
     const int64_t dyn = std::min<int64_t>((share - table) & ~int64_t(255), int64_t(lds_wg) - table);
     plan->restore_lds = n < 4 && dyn > 0 ? uint32_t(dyn) : 0;

@@ -112,7 +112,10 @@ struct HostPlan {
 // the mixed tags, 765-771 / 827-838 / 838-846 for K4V4: the best count falls
 // as units grow.  With no shift (no rotation, no table) the same unaligned
 // plans run best with fewer: mixed 900 / 961 / 978, K8V8 876 / 958 / 967,
-// K8V4 835-839 / 914-918 / 925, K4V4 820 / 802 / 836-842.
+// K8V4 835-839 / 914-918 / 925, K4V4 820 / 802 / 836-842; and so do the
+// shifted ones into separate K and V caches: mixed 968-973 / 1004-1013 /
+// 1032, K8V8 949 / 1019-1022 / 1026-1033, K8V4 910-916 / 945-948 / 972,
+// K4V4 935-939 / 847-848 / 876-878.
 int restore_workgroups_per_cu(const HostPlan& hp);
 
 // Validate and build the host side of a plan.  Makes no HIP call.

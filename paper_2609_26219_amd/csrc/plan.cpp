@@ -128,14 +128,16 @@ bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache
 int restore_workgroups_per_cu(const HostPlan& hp) {
   // The memory system streams best with about 32K output elements of work in
   // flight per compute unit (two thirds of that for read-heavy plans, six
-  // fifths for write-heavy ones, three quarters for units that do not rotate
-  // their keys): so many units at a time, two to four.
+  // fifths for write-heavy ones; three quarters for units that do not rotate
+  // their keys, and again for separate K and V caches): so many units at a
+  // time, two to four.
   const pkv_plan_info_t& info = hp.info;
   if (info.num_units == 0 || info.bytes_written == 0 || info.restored_rows == 0) return 4;
   const double ratio = double(info.bytes_read) / double(info.bytes_written);
   const double rotated = double(hp.rotated_rows) / double(info.restored_rows);
   const double target =
-      32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 1.2) * (0.75 + 0.25 * rotated);
+      32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 1.2) * (0.75 + 0.25 * rotated) *
+      (hp.model.kv_layout == PKV_KV_SEPARATE ? 0.75 : 1.0);
   const double unit_elems =
       double(info.restored_rows) * hp.model.num_kv_heads * hp.model.head_dim / double(info.num_units);
   const double n = std::floor(target / unit_elems + 0.5);

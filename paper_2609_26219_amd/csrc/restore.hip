@@ -18,14 +18,16 @@
 // unit's one page comes with its work item, so no workgroup-wide staging or
 // barrier is needed except for the per-request cos/sin table.  An LDS claim caps
 // the workgroups sharing a compute unit at two to four, chosen per plan from
-// its read:write byte ratio.
+// its read:write byte ratio, its unit size, whether its keys rotate and the
+// cache layout (restore_workgroups_per_cu).
 //
 // Cache layouts.  With separate caches a page's K slots and V slots sit in
 // two buffers; with paired pages they are one contiguous run, K then V.
 // Both are addressed as page << page_shift slot rows from the layer's start.
 //
 // Arithmetic.  Codes decode exactly.  Keys are rotated in double precision
-// (full rate on CDNA4) with a double (cos, sin) table, so the rotated value
+// (v_fma_f64 issues at the rate of v_fma_f32 on CDNA4; an f32 rotation
+// measured no faster) with a double (cos, sin) table, so the rotated value
 // carries ~2^-53 relative error even under cancellation; values use one
 // single-precision FMA.  Results go to float, then to the cache dtype with
 // the hardware round-to-nearest-even conversions.

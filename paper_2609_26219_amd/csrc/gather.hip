@@ -295,8 +295,9 @@ __device__ void encode_tile(const GatherArgs& a, const Unit& u, int which, int h
 
 template <bool BF16, int NL>
 __global__ __launch_bounds__(kGatherMaxWaves * 64, GATHER_MIN_WAVES) void gather_kernel(GatherArgs a) {
-  const Unit u = a.units[blockIdx.x >> 1];
-  const int which = blockIdx.x & 1;
+  const int64_t g = xcd_grouped(blockIdx.x, gridDim.x);
+  const Unit u = a.units[g >> 1];
+  const int which = int(g & 1);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nwaves = blockDim.x >> 6;
@@ -514,7 +515,8 @@ __global__ __launch_bounds__(kGatherMaxWaves * 64) void gather_tile_kernel(TileA
   const int r = lane / a.lpr;
   const int c = lane - r * a.lpr;
   const bool on = r < a.rpl;
-  const int64_t T = int64_t(blockIdx.x) * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t T =
+      xcd_grouped(blockIdx.x, gridDim.x) * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (T >= s.num_tiles) return;
   const TileHdr h = tile_header(a, units, T);
   uint4 w[NL];

@@ -11,6 +11,21 @@
 namespace pkv {
 
 constexpr int kMaxHeadDim = 512;
+
+// The hardware deals a launch's workgroups to the eight XCDs in turn
+// (workgroup b runs on XCD b % 8), each XCD with its own L2.  Kernels take
+// their work item from xcd_grouped(b, grid), which renumbers the workgroups
+// so that kXcdGroup consecutive work items run on one XCD and share its L2
+// (neighbouring payload tiles, scale lines, work items).  It is a permutation
+// of [0, grid); the last, partial round of 8 * kXcdGroup keeps its order.
+constexpr int64_t kXcdCount = 8;
+constexpr int64_t kXcdGroup = 8;
+constexpr int64_t xcd_grouped(int64_t b, int64_t grid) {
+  const int64_t round = kXcdCount * kXcdGroup;
+  if (b >= grid / round * round) return b;
+  const int64_t slot = b / kXcdCount;
+  return slot / kXcdGroup * round + (b % kXcdCount) * kXcdGroup + slot % kXcdGroup;
+}
 constexpr int kMaxRowElems = 4096;   // num_kv_heads * head_dim
 constexpr int kMaxBlockTokens = 1024;
 constexpr int kWorkgroup = 256;       // threads per workgroup

@@ -367,7 +367,7 @@ __device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u,
 template <bool BF16, int STYLE>
 __global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(KernelArgs a) {
   __shared__ __attribute__((aligned(16))) double s_tab[kMaxHeadDim];
-  const Unit u = a.units[blockIdx.x];
+  const Unit u = a.units[xcd_grouped(blockIdx.x, gridDim.x)];
   const int tid = threadIdx.x;
   const int tag = u.tag & 0xFF;
   const bool rot = (u.tag & kUnitRotate) != 0;

@@ -10,6 +10,7 @@ written exactly once and nothing else is written.
 Keep the constants below in step with the kernel's launch code.
 """
 import ctypes
+import os
 
 import numpy as np
 import pytest
@@ -184,3 +185,50 @@ def _paired(case):
 ], ids=["tiny", "h3_d128", "h8_b4_two_requests", "h8_d128_unaligned", "b64_p4"])
 def test_kernel_addresses_paired_pages(maker):
     emulate(maker())
+
+
+_XCD_PROGRAM = r"""
+#include <cstdio>
+#include <vector>
+#include "pkv_internal.h"
+int main() {
+  using pkv::xcd_grouped;
+  const long long grids[] = {0, 1, 7, 8, 63, 64, 65, 127, 128, 129, 1000, 83520, 83521, 131072, 1331936};
+  for (long long grid : grids) {
+    std::vector<long long> phys(grid, -1);
+    for (long long b = 0; b < grid; ++b) {
+      const long long l = xcd_grouped(b, grid);
+      if (l < 0 || l >= grid || phys[l] != -1) { printf("grid %lld: not a permutation at %lld\n", grid, b); return 1; }
+      phys[l] = b;
+    }
+    const long long round = pkv::kXcdCount * pkv::kXcdGroup, full = grid / round * round;
+    for (long long l = 0; l < grid; ++l) {
+      const long long first = l / pkv::kXcdGroup * pkv::kXcdGroup;
+      if (l < full && phys[l] % pkv::kXcdCount != phys[first] % pkv::kXcdCount) {
+        printf("grid %lld: item %lld not on the XCD of item %lld\n", grid, l, first); return 1;
+      }
+      if (l >= full && phys[l] != l) { printf("grid %lld: tail item %lld moved\n", grid, l); return 1; }
+    }
+  }
+  printf("ok\n");
+  return 0;
+}
+"""
+
+
+def test_xcd_grouping_is_a_permutation(tmp_path):
+    """Work items are renumbered so that kXcdGroup consecutive ones share an
+    XCD (workgroup b runs on XCD b % 8); every launch size must still see
+    each work item exactly once."""
+    import shutil
+    import subprocess
+    if shutil.which("g++") is None:
+        pytest.skip("no host C++ compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    src = tmp_path / "xcd.cpp"
+    src.write_text(_XCD_PROGRAM)
+    exe = tmp_path / "xcd"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-I", os.path.join(root, "include"), "-I",
+                    os.path.join(root, "paper_2609_26219_amd", "csrc"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert out.returncode == 0 and out.stdout.strip() == "ok", out.stdout + out.stderr

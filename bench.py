@@ -128,6 +128,8 @@ def cpu_baseline(case, max_workers: int = 16, target_layers: int = 32):
     write_cpu = sum(t for _, t in per_layer)
     rounds = -(-len(layers) // workers)
     wall = restore_cpu / len(layers) * rounds
+    # One layer in this process alone: the single-worker rate, free of the pool's memory contention.
+    one_layer_s, _ = _oracle_layer((0, 0))
     per_layer_bytes = case.algorithmic_bytes()["total"] / case.shape.num_layers
     sample_bytes = per_layer_bytes * len(layers)
     return {
@@ -141,7 +143,22 @@ def cpu_baseline(case, max_workers: int = 16, target_layers: int = 32):
                   f"in value",
         "us_per_restore_extrapolated": round(wall / len(layers) * case.shape.num_layers * 1e6, 1),
         "checkpoint_write_cpu_s_per_layer": round(write_cpu / len(layers), 3),
+        "restore_s_per_layer_in_pool": round(restore_cpu / len(layers), 3),
+        "restore_s_one_layer_one_worker": round(one_layer_s, 3),
+        "one_worker_GBps": round(per_layer_bytes / one_layer_s / 1e9, 4),
+        "cpu_model": _cpu_model(),
     }
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 # ---------------------------------------------------------------------------
@@ -379,6 +396,44 @@ def other_layout(torch, wl, case, dr, stream, steps: int = 20):
     }
 
 
+def small_restores(torch, wl, layout: int, stream, n: int = 50):
+    """The configurations whose working set fits the 256 MB MALL (Tiny, one
+    8B-shaped layer): per-launch time warm (back to back) and cold (a 1 GiB
+    scratch write before each launch, outside its events, so no byte of the
+    restore's inputs or outputs is left in the MALL)."""
+    from paper_2609_26219_amd.device import DeviceRestore
+
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    out = {}
+    for name in ("tiny", "llama8b_1l"):
+        case = wl.make_case(name)
+        case.shape = dataclasses.replace(case.shape, kv_layout=layout)
+        dr = DeviceRestore(case)
+        info = dr.info
+        nbytes = info["bytes_read"] + info["bytes_written"]
+        warm, _ = time_launches(torch, lambda i: dr.run(stream), n, 5, stream)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for i in range(n):
+            scratch.fill_(i & 0xFF)
+            ev[i][0].record(stream)
+            dr.run(stream)
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        cold = sorted(a.elapsed_time(b) for a, b in ev)
+        row = {"algorithmic_bytes": nbytes, "launches": n}
+        for label, ms in (("warm", warm), ("cold", cold)):
+            avg = sum(ms) / len(ms)
+            row[f"us_{label}"] = round(avg * 1e3, 2)
+            row[f"us_{label}_p50"] = round(ms[len(ms) // 2] * 1e3, 2)
+            row[f"GBps_{label}"] = round(nbytes / (avg * 1e-3) / 1e9, 1)
+        log(f"[bench] {name}: {row['us_warm']} us warm, {row['us_cold']} us cold")
+        out[name] = row
+        del dr
+    del scratch
+    torch.cuda.empty_cache()
+    return out
+
+
 def copy_reference(torch, nbytes: int = 4 << 30, reps: int = 10):
     """Plain device-to-device copy (read + write bytes / time): the practical ceiling."""
     src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -415,6 +470,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ref", action="store_true")
     ap.add_argument("--no-other-layout", action="store_true", help="skip timing the restore on the other cache layout")
+    ap.add_argument("--no-small", action="store_true", help="skip the warm/cold Tiny and one-layer restores")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -530,6 +586,8 @@ def main():
         out["other_kv_layout"] = other_layout(torch, wl, case, sets[0], stream)
     if args.host_steps > 0:
         out["host_restore"] = host_restore(torch, binding, sets[0], args.host_steps, stream)
+    if not args.no_small:
+        out["small_restores"] = small_restores(torch, wl, layout, stream)
     if not args.no_representations:
         del sets[1:]
         torch.cuda.empty_cache()

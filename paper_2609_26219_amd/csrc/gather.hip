@@ -381,6 +381,13 @@ __device__ __forceinline__ TileHdr tile_header(const GatherArgs& a, const Unit* 
   return h;
 }
 
+// Cache policy of the tile kernel's buffer loads and stores: non-temporal
+// (the intrinsics' cache-policy operand, nt on gfx950).  Cache rows are read
+// once and the checkpoint is written once, for a later launch; measured 7%
+// faster than the default policy on the 8B-shaped 32-layer write (nt stores
+// alone 5%, nt loads alone 2%).
+constexpr int kNonTemporal = 2;
+
 // Every lane loads every one of its NL rows; rows past n_valid (and idle
 // lanes) read the block's first row instead, so the loads carry no branch and
 // stay in flight together.  Offsets are 32-bit from the tile's base (the
@@ -401,7 +408,7 @@ __device__ __forceinline__ void load_tile(const GatherArgs& a, const TileHdr& h,
     const uint32_t page = uint32_t(h.page0) + (k >= 1 ? uint32_t(h.page1 - h.page0) : 0u) +
                           (k >= 2 ? uint32_t(h.page2 - h.page1) : 0u);
     const uint32_t off = ((page << a.page_shift) | (pos & slot_mask)) * row_bytes + 16u * uint32_t(c);
-    w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0));
+    w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kNonTemporal));
   }
 }
 
@@ -479,7 +486,7 @@ __device__ __forceinline__ void tile_store(const GatherArgs& a, const TileHdr& h
     for (int i = 0; i < NL; ++i) {
       const int t = i * a.rpl + r;
       const uint32_t off = on && t < a.B ? (uint32_t(t) * H + uint32_t(h.head)) * D * 2 + 16u * uint32_t(c) : kDropOffset;
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w[i]), out, off, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w[i]), out, off, 0, kNonTemporal);
     }
     if (lane0) *h.scale_word = 0u;
     return;
@@ -496,12 +503,12 @@ __device__ __forceinline__ void tile_store(const GatherArgs& a, const TileHdr& h
                            encode_word<BF16, 4>(make_uint4(x.z, x.w, 0, 0), q));
       v = valid ? v : make_uint2(0, 0);
       const uint32_t off = store ? (uint32_t(t) * H + uint32_t(h.head)) * D + 8u * uint32_t(c) : kDropOffset;
-      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), out, off, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), out, off, 0, kNonTemporal);
     } else {
       uint32_t v = encode_word<BF16, 8>(x, q);
       v = valid ? v : 0u;
       const uint32_t off = store ? (uint32_t(t) * H + uint32_t(h.head)) * (D / 2) + 4u * uint32_t(c) : kDropOffset;
-      __builtin_amdgcn_raw_buffer_store_b32(v, out, off, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(v, out, off, 0, kNonTemporal);
     }
   }
   if (lane0) *h.scale_word = uint32_t(sb) | (uint32_t(zb) << 16);

@@ -161,6 +161,71 @@ def _cpu_model() -> str:
     return "unknown"
 
 
+def oracle_parity(case, dr, layers) -> dict:
+    """Parity of the timed restore with the oracle, on sampled layers of
+    request 0 (part of the CPU-baseline leg, the only part of the benchmark
+    that calls the oracle).  For each sampled layer: the GPU-written
+    checkpoint against the quantize oracle's, byte for byte; every restored
+    element against the restore oracle's exact value from the oracle's
+    checkpoint, in steps of the output format; and, over every layer, each
+    element the restore must not write against the cache's pre-fill."""
+    import numpy as np
+
+    import oracle
+    from oracle import quantize as oq
+
+    s = case.shape
+    req = case.requests[0]
+    one = dataclasses.replace(req, payload_offset=0, scale_offset=0)
+    s1 = dataclasses.replace(s, num_layers=1)
+    blocks = oracle.reused_blocks(req)
+    layout = oracle.block_layout(req.tags, s.block_tokens, s.num_kv_heads, s.head_dim)
+    slots = np.concatenate([oracle.destination_slots(s, req, b) for b in blocks])
+
+    def ordered(bits):
+        b = bits.astype(np.int32)
+        return np.where(b & 0x8000, -(b & 0x7FFF), b)
+
+    ckpt_bad = n = n_exact = max_ulp = n_nan = 0
+    max_abs_unit = 0.0
+    for layer in layers:
+        _, kb, vb = case.suffix_bits(0, layer)
+        pb, sb = oq.quantize_rows(s, req, kb, vb)
+        po, so = case.layer_payload_offset(0, layer), case.layer_scale_offset(0, layer)
+        ckpt_bad += int((dr.payload[po:po + pb.size].cpu().numpy() != pb).sum())
+        ckpt_bad += int((dr.scales[so:so + sb.size].cpu().numpy().view(np.uint16) != sb.reshape(-1)).sum())
+        got = (dr.rows(0, layer, slots), dr.rows(1, layer, slots))
+        pos = 0
+        for b in blocks:
+            _, k, v = oracle.restore_block(pb, sb.reshape(-1), s1, one, 0, b, layout)
+            m = k.shape[0]
+            for g, exact in ((got[0][pos:pos + m], k), (got[1][pos:pos + m], v)):
+                want = oracle.round_to_output(exact, s.out_dtype)
+                d = np.abs(ordered(g) - ordered(want))
+                n += d.size
+                n_exact += int((g == want).sum())
+                max_ulp = max(max_ulp, int(d.max()))
+                vals = ((g.astype(np.uint32) << 16).view(np.float32).astype(np.float64) if s.out_dtype
+                        else g.view(np.float16).astype(np.float64))
+                n_nan += int(np.isnan(vals).sum())
+                unit = np.abs(exact) < 8.0
+                if unit.any():
+                    max_abs_unit = max(max_abs_unit, float(np.abs(vals - exact)[unit].max()))
+            pos += m
+    untouched_bad = dr.untouched_mismatches(oracle.written_slots(s, case.requests))
+    return {
+        "sample": f"request 0, layers {list(layers)} of {s.num_layers}: {len(blocks)} reused blocks per layer, "
+                  f"{n} restored elements; untouched elements checked in all {s.num_layers} layers",
+        "checkpoint_byte_mismatches": ckpt_bad,
+        "max_ulp": max_ulp,
+        "bit_identical_fraction": round(n_exact / max(1, n), 7),
+        "max_abs_err_unit_scale": max_abs_unit,
+        "nan_outputs": n_nan,
+        "untouched_mismatches": int(untouched_bad),
+        "pass": bool(ckpt_bad == 0 and max_ulp <= 1 and n_nan == 0 and untouched_bad == 0),
+    }
+
+
 # ---------------------------------------------------------------------------
 
 
@@ -582,6 +647,12 @@ def main():
             },
         },
     }
+    parity = None
+    if not args.no_cpu_baseline:
+        parity = oracle_parity(case, sets[0], (0, case.shape.num_layers - 1))
+        log(f"[bench] oracle parity: max ulp {parity['max_ulp']}, bit-identical {parity['bit_identical_fraction']}, "
+            f"checkpoint mismatches {parity['checkpoint_byte_mismatches']}, untouched mismatches "
+            f"{parity['untouched_mismatches']}")
     if not args.no_other_layout:
         out["other_kv_layout"] = other_layout(torch, wl, case, sets[0], stream)
     if args.host_steps > 0:
@@ -605,6 +676,7 @@ def main():
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(case)
+        out["cpu_baseline"]["oracle_parity"] = parity
     print(json.dumps(out), flush=True)
 
 

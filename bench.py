@@ -103,9 +103,19 @@ def _oracle_layer(args):
     t_write = time.perf_counter() - t
     one = dataclasses.replace(req, payload_offset=0, scale_offset=0)
     s1 = dataclasses.replace(case.shape, num_layers=1)
-    cache = np.zeros((1, s1.pool_pages, s1.page_size, s1.num_kv_heads, s1.head_dim), np.uint16)
+    H, D = s1.num_kv_heads, s1.head_dim
+    k_cache = np.zeros((s1.pool_pages * s1.page_size, H, D), np.uint16)
+    v_cache = np.zeros_like(k_cache)
+    scales = sb.reshape(-1)
+    # The oracle's restore body, block by block, into the caches in place
+    # (oracle.restore itself first copies both caches, which is not part of
+    # the method and would dominate on a 2^20-slot pool).
     t = time.perf_counter()
-    oracle.restore(s1, [one], pb, sb.reshape(-1), cache, cache)
+    layout = oracle.block_layout(req.tags, s1.block_tokens, H, D)
+    for b in oracle.reused_blocks(one):
+        slots, k, v = oracle.restore_block(pb, scales, s1, one, 0, b, layout)
+        k_cache[slots] = oracle.round_to_output(k, s1.out_dtype)
+        v_cache[slots] = oracle.round_to_output(v, s1.out_dtype)
     return time.perf_counter() - t, t_write
 
 
@@ -159,6 +169,55 @@ def _cpu_model() -> str:
     except OSError:
         pass
     return "unknown"
+
+
+def oracle_configs(max_workers: int = 16, sampled_layers: int = 4) -> dict:
+    """The oracle timed on every named configuration (``--oracle-configs``),
+    one process per (request, layer) job: the one-layer configurations and
+    the 32-layer one in full, the 70B-shaped and batched ones on their first
+    ``sampled_layers`` layers, extrapolated linearly in layers.  The wall
+    estimate assumes the jobs spread evenly over the workers."""
+    from paper_2609_26219_amd import workloads as wl
+
+    global _CPU_CASE
+    try:
+        n_cpu = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n_cpu = os.cpu_count() or 1
+    workers = max(1, min(max_workers, n_cpu))
+    out = {"workers": workers, "cpu_model": _cpu_model()}
+    for name in ("tiny", "llama8b_1l", "llama8b_32l", "llama70b", "batched16"):
+        case = wl.make_case(name)
+        L = case.shape.num_layers
+        layers = list(range(L)) if L <= 32 else list(range(sampled_layers))
+        if name == "batched16":
+            layers = list(range(sampled_layers))
+        jobs = [(ri, l) for ri in range(len(case.requests)) for l in layers]
+        _CPU_CASE = case
+        t = time.perf_counter()
+        with mp.get_context("fork").Pool(min(workers, len(jobs))) as pool:
+            times = pool.map(_oracle_layer, jobs)
+        wall_measured = time.perf_counter() - t
+        restore_cpu = sum(r for r, _ in times)
+        full_cpu = restore_cpu * L / len(layers)
+        est_wall = full_cpu / min(workers, len(jobs) * L // len(layers))
+        nbytes = case.algorithmic_bytes()["total"]
+        out[name] = {
+            "requests": len(case.requests),
+            "layers_timed": len(layers),
+            "layers": L,
+            "extrapolated": len(layers) < L,
+            "restore_cpu_s_timed": round(restore_cpu, 3),
+            "restore_cpu_s_full": round(full_cpu, 3),
+            "est_wall_s": round(est_wall, 4),
+            "GBps": round(nbytes / est_wall / 1e9, 4),
+            "job_mean_s": round(restore_cpu / len(jobs), 4),
+            "sample_wall_s_incl_checkpoint_write": round(wall_measured, 2),
+        }
+        log(f"[bench] oracle {name}: {out[name]['est_wall_s']} s per restore at {workers} workers"
+            f"{' (extrapolated)' if len(layers) < L else ''}, {out[name]['GBps']} GB/s")
+    _CPU_CASE = None
+    return out
 
 
 def oracle_parity(case, dr, layers) -> dict:
@@ -536,7 +595,13 @@ def main():
     ap.add_argument("--no-copy-ref", action="store_true")
     ap.add_argument("--no-other-layout", action="store_true", help="skip timing the restore on the other cache layout")
     ap.add_argument("--no-small", action="store_true", help="skip the warm/cold Tiny and one-layer restores")
+    ap.add_argument("--oracle-configs", action="store_true",
+                    help="only time the CPU oracle on every named configuration and print that as JSON")
     args = ap.parse_args()
+
+    if args.oracle_configs:
+        print(json.dumps({"cpu_oracle_configs": oracle_configs()}), flush=True)
+        return
 
     if args.gpus != 1:
         print(f"bench.py: this build restores on one GPU only; --gpus {args.gpus} is not supported "

@@ -97,7 +97,7 @@ typedef enum { PKV_OUT_FP16 = 0, PKV_OUT_BF16 = 1 } pkv_out_dtype_t;
 typedef enum { PKV_ROPE_HALF = 0, PKV_ROPE_INTERLEAVED = 1 } pkv_rope_style_t;
 
 /* Paged KV cache layout (see "caches" above).  PKV_KV_PAIRED keeps a page's K
- * and V slots in one contiguous run; on MI355X the restore writes it about 7%
+ * and V slots in one contiguous run; on MI355X the restore writes it 5-7%
  * faster than two separate caches. */
 typedef enum { PKV_KV_SEPARATE = 0, PKV_KV_PAIRED = 1 } pkv_kv_layout_t;
 

@@ -604,7 +604,7 @@ def main():
         return
 
     if args.gpus != 1:
-        print(f"bench.py: this build restores on one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the restore is measured on one GPU; --gpus {args.gpus} is not supported "
               f"(the restore shards by request, layer or KV head with no exchange step).", file=sys.stderr)
         sys.exit(2)
 

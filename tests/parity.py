@@ -1,6 +1,6 @@
 """Element-by-element comparison of GPU cache rows with the CPU oracle.
 
-Tolerance (stated by the task's parity bar): every restored element within
+Tolerance: every restored element within
 one unit in the last place of the oracle's exactly rounded value (both
 neighbours of a near-tie are correct: the kernel rounds double -> float ->
 cache dtype); for fp16 output, max |GPU - exact| <= 2e-3 over unit-scale

@@ -38,8 +38,12 @@ def test_checkpoint_bit_exact_named(name, int4, torch):
     # blocks spanning more than three pages: the general kernel with 4 and 2 loads per lane
     dict(L=1, H=4, D=64, B=32, P=8, n_tokens=(77,), deltas=(1,), rho0s=(6,), out_dtype=wl.OUT_BF16),
     dict(L=2, H=2, D=32, B=16, P=4, n_tokens=(45, 16), deltas=(0, 3), rho0s=(2, 9), out_dtype=wl.OUT_FP16),
+    # 70B-shaped blocks (64 tokens, 32-token pages): 16 loads per lane in the tile kernel with 8 waves;
+    # with 12 heads the workgroup is too large for it and the general kernel takes 16 loads in one pass
+    dict(L=2, H=8, D=128, B=64, P=32, n_tokens=(150, 64), deltas=(4096, 0), rho0s=(31, 96), out_dtype=wl.OUT_BF16),
+    dict(L=1, H=12, D=128, B=64, P=32, n_tokens=(130,), deltas=(-7,), rho0s=(17,), out_dtype=wl.OUT_BF16),
 ], ids=["bf16_two_requests", "b64_bf16", "h3_three_requests_fp16", "d256_b8", "d512_b64_streamed_twice",
-        "h20_d16", "d48_idle_lanes", "general_nl4", "general_nl2"])
+        "h20_d16", "d48_idle_lanes", "general_nl4", "general_nl2", "h8_b64_p32_tile16", "h12_b64_general16"])
 def test_checkpoint_bit_exact_custom(params, torch):
     case = wl.make_custom(11, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), outlier_pairs=1, **params)
     check_checkpoint_write(case, torch)
@@ -49,7 +53,8 @@ def test_checkpoint_bit_exact_custom(params, torch):
     dict(L=2, H=2, D=64, B=16, P=16, n_tokens=(100, 40), deltas=(5, -3), rho0s=(20, 7), out_dtype=wl.OUT_BF16),
     dict(L=2, H=8, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,), out_dtype=wl.OUT_BF16),
     dict(L=1, H=4, D=64, B=32, P=8, n_tokens=(77,), deltas=(1,), rho0s=(6,), out_dtype=wl.OUT_FP16),
-], ids=["two_requests", "h8_d128", "general_kernel"])
+    dict(L=1, H=8, D=128, B=64, P=32, n_tokens=(150,), deltas=(4096,), rho0s=(31,), out_dtype=wl.OUT_BF16),
+], ids=["two_requests", "h8_d128", "general_kernel", "h8_b64_p32_tile16"])
 def test_checkpoint_bit_exact_paired_pages(params, torch):
     import dataclasses
     case = wl.make_custom(12, tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), outlier_pairs=1, **params)

@@ -181,9 +181,13 @@ def test_gather_addresses_paired_pages(maker):
                            tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
     lambda: wl.make_custom(8, L=1, H=20, D=16, B=8, P=8, n_tokens=(21,), deltas=(1,), rho0s=(3,),
                            tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
-], ids=["tiny", "h8_b4_two_requests", "h4_d64_b64", "h8_d128", "h20_heads_loop"])
+    # 70B-shaped blocks: 64 tokens over 32-token pages, 16 loads per lane in 8-wave workgroups
+    lambda: wl.make_custom(13, L=1, H=8, D=128, B=64, P=32, n_tokens=(150, 64), deltas=(4096, 0), rho0s=(31, 96),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+], ids=["tiny", "h8_b4_two_requests", "h4_d64_b64", "h8_d128", "h20_heads_loop", "h8_d128_b64_p32"])
 def test_tile_kernel_tiles_and_pages(maker):
-    """Tile kernel (blocks of at most 2P + 1 tokens, at most 8 loads per lane):
+    """Tile kernel (blocks of at most 2P + 1 tokens, at most 8 loads per lane,
+    16 with workgroups of at most 8 waves):
     wave w of workgroup b encodes tile b * waves + w of the (unit, K|V, head)
     order, so a grid of ceil(tiles / waves) workgroups encodes every tile
     exactly once; the three source pages carried in each unit give every
@@ -206,7 +210,7 @@ def test_tile_kernel_tiles_and_pages(maker):
     lpr = D // 8
     rpl = 64 // lpr
     nload = -(-B // rpl)
-    assert loads_per_chunk(nload) <= 8 and loads_per_chunk(nload) >= nload
+    assert loads_per_chunk(nload) <= (16 if WG <= 512 else 8) and loads_per_chunk(nload) >= nload
     for u in units:
         pages = [int(u["table_off"]), int(u["page1"]), int(u["page2"])]  # page0 shares table_off's slot
         first = int(u["row0"]) // P

@@ -114,8 +114,9 @@ struct HostPlan {
   int64_t rotated_rows = 0;  // restore plans: restored rows whose keys rotate (shift != 0)
 };
 
-// Restore workgroups resident per compute unit (one wave per SIMD each; four
-// is the register limit), chosen per plan.  Measured on the 8B-shaped
+// Restore workgroups resident per compute unit, chosen per plan: 8 to 16
+// waves (for 4-wave workgroups two to four, one wave per SIMD each; 16 waves
+// is the register limit).  Measured on the 8B-shaped
 // 32-layer restore, paired pages, destination rows 7 slots into a page
 // (units of 9, 16 and 7 tokens), us for 2/3/4:
 //   FP16 (read:write 1.00)  1227-1235 / 1277 / 1282-1290
@@ -178,6 +179,7 @@ uint64_t layer_payload_bytes(const pkv_model_t& m, const uint8_t* tags, int64_t 
 
 // Tokens per unit for a model: about kUnitElems output elements, at most one block.
 int32_t unit_tokens(const pkv_model_t& m);
+int32_t restore_workgroup(const pkv_model_t& m);
 
 // Cache geometry by layout.  A page's slots start at page << page_shift slot
 // rows from the layer's start (log2 P, plus one when a page holds its K and V

@@ -130,9 +130,9 @@ int restore_workgroups_per_cu(const HostPlan& hp) {
   // flight per compute unit (two thirds of that for read-heavy plans, six
   // fifths for write-heavy ones; three quarters for units that do not rotate
   // their keys, and again for separate K and V caches): so many units at a
-  // time, two to four.
+  // time, between 8 and 16 waves' worth (two to four 4-wave workgroups).
   const pkv_plan_info_t& info = hp.info;
-  if (info.num_units == 0 || info.bytes_written == 0 || info.restored_rows == 0) return 4;
+  if (info.num_units == 0 || info.bytes_written == 0 || info.restored_rows == 0) return std::max(1, 16 / std::max(1, hp.workgroup / 64));
   const double ratio = double(info.bytes_read) / double(info.bytes_written);
   const double rotated = double(hp.rotated_rows) / double(info.restored_rows);
   const double target =
@@ -141,7 +141,21 @@ int restore_workgroups_per_cu(const HostPlan& hp) {
   const double unit_elems =
       double(info.restored_rows) * hp.model.num_kv_heads * hp.model.head_dim / double(info.num_units);
   const double n = std::floor(target / unit_elems + 0.5);
-  return n < 2 ? 2 : n > 4 ? 4 : int(n);
+  const int waves = std::max(1, hp.workgroup / 64);
+  const int lo = std::max(1, 8 / waves), hi = std::max(1, 16 / waves);
+  return n < lo ? lo : n > hi ? hi : int(n);
+}
+
+// Threads of a restore workgroup: enough that each thread owns at most four
+// tokens of the largest unit (units stop at page ends), in whole waves, at
+// most kWorkgroup.  Rows of 8 heads x 128 keep 256; a one-head row of 128
+// takes one wave, so shards with few heads per GPU do not leave most of each
+// workgroup idle.
+int32_t restore_workgroup(const pkv_model_t& m) {
+  const int64_t cols = int64_t(m.num_kv_heads) * m.head_dim / 16;
+  const int64_t tokens = std::min<int64_t>(unit_tokens(m), m.page_size);
+  const int64_t threads = (cols * ceil_div(tokens, 4) + 63) / 64 * 64;
+  return int32_t(std::max<int64_t>(64, std::min<int64_t>(kWorkgroup, threads)));
 }
 
 int32_t unit_tokens(const pkv_model_t& m) {
@@ -253,6 +267,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
     }
     // Work list, layer-major, and the streamed restore's copy ranges.
     const int64_t per_unit = unit_tokens(m);
+    hp.workgroup = restore_workgroup(m);
     // Append a copy, merging it with the previous one (if that one is at
     // index >= first) when it starts at most `gap` bytes after that one ends.
     auto add_range = [](std::vector<CopyRange>& v, int64_t first, uint64_t off, uint64_t len, uint64_t gap) {
@@ -478,6 +493,13 @@ pkv_status_t pkv_internal_host_units(const pkv_model_t* model, const pkv_request
   *count = int64_t(hp.units.size());
   if (units_out && capacity >= *count && *count > 0)
     memcpy(units_out, hp.units.data(), hp.units.size() * sizeof(pkv::Unit));
+  return PKV_OK;
+}
+
+// Internal test hook (not part of pkv.h): threads per restore workgroup.
+pkv_status_t pkv_internal_restore_workgroup(const pkv_model_t* model, int32_t* threads) {
+  if (!model || !threads) return PKV_ERR_INVALID_ARGUMENT;
+  *threads = pkv::restore_workgroup(*model);
   return PKV_OK;
 }
 

@@ -13,7 +13,8 @@
 // that is a set of whole rotary pairs, so the rotation needs no cross-lane
 // exchange; for keys and values alike, each store instruction of a wave
 // writes whole 128-byte lines.  Threads (t0, c), c = head*(D/16) + j, own
-// tokens t0, t0+tpp, ... with tpp = 256 / (H*D/16) (at most four of them)
+// tokens t0, t0+tpp, ... with tpp = threads / (H*D/16) (at most four of
+// them; a workgroup has 64 to 256 threads, restore_workgroup())
 // and issue the loads of all their tokens before the first store; the
 // unit's one page comes with its work item, so no workgroup-wide staging or
 // barrier is needed except for the per-request cos/sin table.  An LDS claim caps
@@ -377,7 +378,7 @@ __global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(Ker
   const int tag = u.tag & 0xFF;
   const bool rot = (u.tag & kUnitRotate) != 0;
   if (rot) {  // uniform across the workgroup
-    for (int i = tid; i < a.D; i += kWorkgroup) s_tab[i] = a.tables[u.table_off + i];
+    for (int i = tid; i < a.D; i += int(blockDim.x)) s_tab[i] = a.tables[u.table_off + i];
     __syncthreads();
   }
   const int t0 = tid / a.cols;
@@ -437,7 +438,7 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
     const int64_t n = restore_workgroups_per_cu(plan->host);
     const int64_t share = (int64_t(lds_cu) / n + int64_t(lds_cu) / (n + 1)) / 2;
     const int64_t dyn = std::min<int64_t>((share - table) & ~int64_t(255), int64_t(lds_wg) - table);
-    plan->restore_lds = n < 4 && dyn > 0 ? uint32_t(dyn) : 0;
+    plan->restore_lds = n < 16 / std::max(1, plan->host.workgroup / 64) && dyn > 0 ? uint32_t(dyn) : 0;
   } else {
     (void)hipGetLastError();
   }
@@ -543,9 +544,9 @@ pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const voi
   a.D = m.head_dim;
   a.log2P = plan->host.log2_page;
   a.cols = m.num_kv_heads * m.head_dim / 16;
-  a.tpp = kWorkgroup / a.cols;
+  a.tpp = plan->host.workgroup / a.cols;
   a.R = m.rotary_dim ? m.rotary_dim : m.head_dim;
-  const dim3 grid(static_cast<uint32_t>(n)), block(kWorkgroup);
+  const dim3 grid(static_cast<uint32_t>(n)), block(plan->host.workgroup);
   const bool bf16 = m.out_dtype == PKV_OUT_BF16, half = m.rope_style == PKV_ROPE_HALF;
   if (bf16 && half)
     hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_HALF>), grid, block, plan->restore_lds, stream, a);

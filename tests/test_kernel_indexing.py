@@ -19,7 +19,6 @@ import oracle
 from paper_2609_26219_amd import binding as pb
 from paper_2609_26219_amd import workloads as wl
 
-WG = 256  # threads per workgroup
 KBITS = (16, 8, 8, 4)
 VBITS = (16, 8, 4, 4)
 UNIT_ELEMS = 16384  # target output elements per unit
@@ -43,10 +42,22 @@ def host_units(shape, requests):
     return units
 
 
+def restore_workgroup(shape) -> int:
+    fn = pb.load().pkv_internal_restore_workgroup
+    fn.argtypes = [ctypes.POINTER(pb.PkvModel), ctypes.POINTER(ctypes.c_int32)]
+    fn.restype = ctypes.c_int32
+    m = pb.make_model(shape)
+    wg = ctypes.c_int32()
+    assert fn(ctypes.byref(m), ctypes.byref(wg)) == 0
+    return wg.value
+
+
 def emulate(case):
     s = case.shape
     H, D, B, P = s.num_kv_heads, s.head_dim, s.block_tokens, s.page_size
+    WG = restore_workgroup(s)
     cols = H * D // 16
+    assert WG % 64 == 0 and 64 <= WG <= 256
     tpp = WG // cols
     dq = D // 16
     paired = s.kv_layout == wl.KV_PAIRED
@@ -161,9 +172,32 @@ def emulate(case):
                            tag_set=(1, 2), mix=(1, 1), repair_frac=0.0),
     lambda: wl.make_custom(5, L=2, H=8, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,),
                            tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2),
-], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "d256_b64", "h32_b8", "h8_d128_split_units"])
+    # tensor-parallel shards of the 8B shape: 1, 2 and 4 heads per GPU (64-, 64- and 128-thread workgroups)
+    lambda: wl.make_custom(14, L=2, H=1, D=128, B=32, P=16, n_tokens=(75,), deltas=(-1500,), rho0s=(1507,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2),
+    lambda: wl.make_custom(15, L=2, H=2, D=128, B=32, P=16, n_tokens=(75,), deltas=(-3,), rho0s=(7,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2),
+    lambda: wl.make_custom(16, L=1, H=4, D=128, B=32, P=16, n_tokens=(75,), deltas=(5,), rho0s=(13,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2),
+], ids=["tiny", "tiny_k4v4", "h3_d128", "h8_b4_two_requests", "d256_b64", "h32_b8", "h8_d128_split_units",
+        "tp_h1", "tp_h2", "tp_h4"])
 def test_kernel_addresses(maker):
     emulate(maker())
+
+
+@pytest.mark.parametrize("H,D,B,P,want", [
+    (8, 128, 32, 16, 256), (4, 128, 32, 16, 128), (2, 128, 32, 16, 64), (1, 128, 32, 16, 64),
+    (1, 128, 64, 32, 64), (32, 128, 8, 8, 256), (8, 512, 4, 2, 256), (2, 64, 16, 16, 64), (3, 128, 32, 16, 128),
+])
+def test_restore_workgroup_size(H, D, B, P, want):
+    """Each thread owns at most four tokens of the largest unit (units stop at
+    page ends), in whole waves, 64 to 256 threads."""
+    case = wl.make_custom(1, L=1, H=H, D=D, B=B, P=P, n_tokens=(B,), deltas=(0,), rho0s=(0,))
+    wg = restore_workgroup(case.shape)
+    assert wg == want
+    cols = H * D // 16
+    unit = min(max(1, min(B, UNIT_ELEMS // (H * D))), P)
+    assert -(-unit // (wg // cols)) <= 4
 
 
 def _paired(case):
@@ -182,7 +216,9 @@ def _paired(case):
                                    tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2)),
     lambda: _paired(wl.make_custom(6, L=1, H=2, D=64, B=64, P=4, n_tokens=(130,), deltas=(1,), rho0s=(3,),
                                    tag_set=(0, 2), mix=(1, 1), repair_frac=0.1)),
-], ids=["tiny", "h3_d128", "h8_b4_two_requests", "h8_d128_unaligned", "b64_p4"])
+    lambda: _paired(wl.make_custom(14, L=2, H=1, D=128, B=32, P=16, n_tokens=(75,), deltas=(-1500,), rho0s=(1507,),
+                                   tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1), repair_frac=0.2)),
+], ids=["tiny", "h3_d128", "h8_b4_two_requests", "h8_d128_unaligned", "b64_p4", "tp_h1"])
 def test_kernel_addresses_paired_pages(maker):
     emulate(maker())
 

@@ -90,6 +90,9 @@ PROPERTY_CASES = [
     (16, 32, 256, 2, (45,), (-8192,), (17,), (0, 2), 0.0, wl.OUT_FP16),
     (32, 16, 128, 3, (70,), (12,), (9,), (0, 1, 2, 3), 0.0, wl.OUT_BF16),  # H*D/16 = 24 (idle lanes)
     (4, 16, 128, 8, (23,), (5,), (2,), (0, 1, 2, 3), 0.2, wl.OUT_FP16),
+    # tensor-parallel shards of the 8B shape: one-wave workgroups, two and four tokens per thread
+    (32, 16, 128, 1, (300, 77), (-1500, 0), (1507, 5), (0, 1, 2, 3), 0.15, wl.OUT_BF16),
+    (32, 16, 128, 2, (190,), (-1500,), (1509,), (0, 1, 2, 3), 0.15, wl.OUT_BF16),
 ]
 
 

@@ -132,7 +132,9 @@ int restore_workgroups_per_cu(const HostPlan& hp) {
   // their keys, and again for separate K and V caches): so many units at a
   // time, between 8 and 16 waves' worth (two to four 4-wave workgroups).
   const pkv_plan_info_t& info = hp.info;
-  if (info.num_units == 0 || info.bytes_written == 0 || info.restored_rows == 0) return std::max(1, 16 / std::max(1, hp.workgroup / 64));
+  const int waves = std::max(1, hp.workgroup / 64);
+  const int lo = std::max(1, 8 / waves), hi = std::max(1, 16 / waves);
+  if (info.num_units == 0 || info.bytes_written == 0 || info.restored_rows == 0) return hi;
   const double ratio = double(info.bytes_read) / double(info.bytes_written);
   const double rotated = double(hp.rotated_rows) / double(info.restored_rows);
   const double target =
@@ -141,8 +143,6 @@ int restore_workgroups_per_cu(const HostPlan& hp) {
   const double unit_elems =
       double(info.restored_rows) * hp.model.num_kv_heads * hp.model.head_dim / double(info.num_units);
   const double n = std::floor(target / unit_elems + 0.5);
-  const int waves = std::max(1, hp.workgroup / 64);
-  const int lo = std::max(1, 8 / waves), hi = std::max(1, 16 / waves);
   return n < lo ? lo : n > hi ? hi : int(n);
 }
 

@@ -248,6 +248,18 @@ def test_llama8b_32l_full_size_paired_pages(torch):
     log(f"  {st}")
 
 
+@pytest.mark.parametrize("heads", [1, 2])
+def test_tensor_parallel_share_full_size(heads, torch):
+    """One GPU's share of the 8B-shaped workload under tensor parallelism over
+    KV heads (1 or 2 heads per GPU: one-wave workgroups), at full length."""
+    log(f"[gpu] 8B-shaped share with {heads} KV head(s): full-size checkpoint + restore, 2 sampled layers")
+    case = wl.make_custom(41, L=32, H=heads, D=128, B=32, P=16, n_tokens=(32768,), deltas=(-1500,), rho0s=(5007,),
+                          mix=(0.7, 0.2, 0.1), tag_set=(wl.TAG_K8V4, wl.TAG_K8V8, wl.TAG_FP16), repair_frac=0.15,
+                          out_dtype=wl.OUT_BF16, theta=5e5, outlier_pairs=1)
+    st = _full_size(_paired(case), [(0, 0), (0, 31)], torch)
+    log(f"  {st}")
+
+
 def test_llama70b_full_size(torch):
     log("[gpu] llama70b: full-size checkpoint + restore, 2 sampled layers + untouched check")
     _full_size(wl.make_case("llama70b", distinct_layers=2), [(0, 1), (0, 78)], torch)

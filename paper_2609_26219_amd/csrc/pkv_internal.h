@@ -131,7 +131,9 @@ struct HostPlan {
 // K8V4 835-839 / 914-918 / 925, K4V4 820 / 802 / 836-842; and so do the
 // shifted ones into separate K and V caches: mixed 968-973 / 1004-1013 /
 // 1032, K8V8 949 / 1019-1022 / 1026-1033, K8V4 910-916 / 945-948 / 972,
-// K4V4 935-939 / 847-848 / 876-878.
+// K4V4 935-939 / 847-848 / 876-878.  The one-head-per-GPU share of the same
+// workload restores in 139 us (16 one-wave workgroups) whatever the target,
+// the two-head share in 263 us at 8 one-wave workgroups and 243 at 12 or 16.
 int restore_workgroups_per_cu(const HostPlan& hp);
 
 // Validate and build the host side of a plan.  Makes no HIP call.

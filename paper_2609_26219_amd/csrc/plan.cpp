@@ -129,7 +129,8 @@ int restore_workgroups_per_cu(const HostPlan& hp) {
   // The memory system streams best with about 32K output elements of work in
   // flight per compute unit (two thirds of that for read-heavy plans, six
   // fifths for write-heavy ones; three quarters for units that do not rotate
-  // their keys, and again for separate K and V caches): so many units at a
+  // their keys, and again for separate K and V caches; half again for rows
+  // narrow enough to take workgroups under 256 threads): so many units at a
   // time, between 8 and 16 waves' worth (two to four 4-wave workgroups).
   const pkv_plan_info_t& info = hp.info;
   const int waves = std::max(1, hp.workgroup / 64);
@@ -139,7 +140,7 @@ int restore_workgroups_per_cu(const HostPlan& hp) {
   const double rotated = double(hp.rotated_rows) / double(info.restored_rows);
   const double target =
       32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 1.2) * (0.75 + 0.25 * rotated) *
-      (hp.model.kv_layout == PKV_KV_SEPARATE ? 0.75 : 1.0);
+      (hp.model.kv_layout == PKV_KV_SEPARATE ? 0.75 : 1.0) * (hp.workgroup < kWorkgroup ? 1.5 : 1.0);
   const double unit_elems =
       double(info.restored_rows) * hp.model.num_kv_heads * hp.model.head_dim / double(info.num_units);
   const double n = std::floor(target / unit_elems + 0.5);

@@ -10,7 +10,7 @@ import numpy as np
 
 from paper_2609_26219_amd import workloads as wl
 
-SWEEP_SIZE = 24
+SWEEP_SIZE = 32
 MAX_ELEMS = 1_500_000  # layers x suffix tokens x heads x head_dim, per case
 
 

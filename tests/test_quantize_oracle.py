@@ -21,8 +21,11 @@ def _ns(**kw):
     return types.SimpleNamespace(**kw)
 
 
-def test_hand_worked_checkpoint_write():
-    d = json.load(open(os.path.join(GOLDEN, "hand_quantize_d4.json")))
+@pytest.mark.parametrize("fixture", ["hand_quantize_d4.json", "hand_quantize_d4_bf16.json"])
+def test_hand_worked_checkpoint_write(fixture):
+    """The binary16 fixture and its bfloat16 twin: same K8V4 values, an FP16
+    block whose bfloat16 values need rounding to binary16 (ties included)."""
+    d = json.load(open(os.path.join(GOLDEN, fixture)))
     s = d["shape"]
     shape = _ns(num_layers=1, num_kv_heads=1, head_dim=4, block_tokens=2, page_size=2, pool_pages=3,
                 out_dtype=s["cache_dtype"])
@@ -30,9 +33,11 @@ def test_hand_worked_checkpoint_write():
     req = _ns(suffix_tokens=r["suffix_tokens"], src_row0=r["src_row0"], tags=np.array(r["tags"], np.uint8),
               src_page_table=np.array(r["page_table"], np.int32), payload_offset=0, scale_offset=0)
     caches = []
+    fill = int(d.get("fill_hex", "7e00"), 16)  # NaN of the cache dtype
+    old = d.get("old_cache_hex") or d["old_cache_f16_hex"]
     for kv in ("k", "v"):
-        c = np.full((1, 3, 2, 1, 4), 0x7E00, dtype=np.uint16).reshape(1, 6, 1, 4)
-        for slot, words in d["old_cache_f16_hex"][kv].items():
+        c = np.full((1, 3, 2, 1, 4), fill, dtype=np.uint16).reshape(1, 6, 1, 4)
+        for slot, words in old[kv].items():
             c[0, int(slot), 0] = [int(w, 16) for w in words]
         caches.append(c.reshape(1, 3, 2, 1, 4))
     payload, scales = oq.quantize_gather(shape, [req], caches[0], caches[1], 44, 8)
@@ -45,6 +50,22 @@ def test_hand_worked_checkpoint_write():
             want += bytes(int(b, 16) for b in seg["u8"])
     assert payload.tobytes() == bytes(want)
     assert [f"{x:04x}" for x in scales] == d["expected_scales_f16_hex"]
+
+
+def test_cache_values_from_literal_bits():
+    """Cache bit patterns decode by their own format's definition (hand-derived
+    values): bfloat16 = sign, 8 exponent bits (bias 127), 7 fraction bits;
+    binary16 = sign, 5 exponent bits (bias 15), 10 fraction bits."""
+    bf = np.array([0x3F80, 0xC000, 0x8000, 0x0001, 0x7F7F, 0x3581, 0x4049, 0x0080], np.uint16)
+    got = oq.cache_values(bf, oq.OUT_BF16)
+    want = [1.0, -2.0, -0.0, 2.0 ** -133, (2 - 2 ** -7) * 2.0 ** 127, (1 + 2 ** -7) * 2.0 ** -20, 3.140625,
+            2.0 ** -126]
+    assert got.tolist() == want
+    assert np.signbit(got[2])
+    hf = np.array([0x3C00, 0xC000, 0x8000, 0x0001, 0x7BFF, 0x3555, 0x0400], np.uint16)
+    got = oq.cache_values(hf, oq.OUT_FP16)
+    assert got.tolist() == [1.0, -2.0, -0.0, 2.0 ** -24, 65504.0, (1 + 0x155 / 1024) * 2.0 ** -2, 2.0 ** -14]
+    assert np.signbit(got[2])
 
 
 def test_fp16_floor_ceil_are_extremal():

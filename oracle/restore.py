@@ -237,6 +237,73 @@ def round_to_output(x: np.ndarray, out_dtype: int) -> np.ndarray:
     return round_fp16_bits(x) if out_dtype == OUT_FP16 else round_bf16_bits(x)
 
 
+def output_values(bits: np.ndarray, out_dtype: int) -> np.ndarray:
+    """fp64 values of fp16 / bf16 output bit patterns."""
+    bits = np.asarray(bits, dtype=np.uint16)
+    if out_dtype == OUT_FP16:
+        return bits.view(np.float16).astype(np.float64)
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+# --------------------------------------------------------------------------
+# Which outputs are correct (reading: several correct results near ties)
+# --------------------------------------------------------------------------
+#
+# The exact result is the one rounding of the fp64 value above.  An
+# implementation that first rounds to single precision and then to the cache
+# dtype can land on the other side of a rounding midpoint m of the cache
+# dtype, but only when the value lies within that first rounding (at most
+# 2^-24 |x|) of m.  Both neighbours of such a near-tie are accepted, and
+# nothing else: away from a midpoint only the exactly rounded value is.
+
+TIE_WINDOW_REL = 2.0 ** -23  # twice half a single-precision ulp, relative to |x|
+
+
+def rotation_slack(exact_k: np.ndarray, delta: int) -> Optional[np.ndarray]:
+    """Absolute slack for rotated keys ``[..., D]`` (``None`` when Delta is 0:
+    no rotation, so the result is a plain rounding).  A rotation computed from
+    a differently rounded angle Delta*f_i (f_i <= 1) and cos/sin differs from
+    this module's by at most about 2^-51 (1 + |Delta|) (|x| + |y|) for the pair
+    (x, y); a rotation keeps each pair's norm, so |x| + |y| <= 2 max|x'| over
+    the head's outputs.  The slack is 4x that bound."""
+    if delta == 0:
+        return None
+    row_max = np.abs(np.asarray(exact_k, dtype=np.float64)).max(axis=-1, keepdims=True)
+    return 2.0 ** -47 * (1.0 + abs(float(delta))) * row_max
+
+
+def classify_outputs(got_bits: np.ndarray, exact: np.ndarray, out_dtype: int,
+                     slack: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """(exactly rounded, accepted near-tie) masks of output bit patterns
+    against exact fp64 values.  An element that is neither is wrong.
+
+    Near-tie: the bits are the other neighbour of the midpoint m between
+    them and the exactly rounded value (the two are adjacent), and
+    ``|x - m| <= 2^-23 |x| + slack``.  ``slack`` (absolute, broadcastable)
+    is given for rotated keys only (:func:`rotation_slack`); for them a zero
+    of either sign is also accepted where the exact result rounds to zero
+    (x*c - y*s can give -0 or +0).  Elsewhere signed zeros must match."""
+    got = np.asarray(got_bits, dtype=np.uint16)
+    x = np.asarray(exact, dtype=np.float64)
+    want = round_to_output(x, out_dtype)
+    same = got == want
+    gv = output_values(got, out_dtype)
+    wv = output_values(want, out_dtype)
+    mid = (gv + wv) / 2.0  # exact in fp64: both are short binary fractions
+    # adjacent: no representable value strictly between them, i.e. their
+    # sign-magnitude orders differ by one
+    def order(b):
+        b = b.astype(np.int32)
+        return np.where(b & 0x8000, -(b & 0x7FFF), b)
+    adjacent = np.abs(order(got) - order(want)) == 1
+    window = TIE_WINDOW_REL * np.abs(x) + (0.0 if slack is None else slack)
+    with np.errstate(invalid="ignore"):
+        near = ~same & adjacent & np.isfinite(gv) & (np.abs(x - mid) <= window)
+    if slack is not None:
+        near |= ~same & (gv == 0.0) & (wv == 0.0)
+    return same, near
+
+
 # --------------------------------------------------------------------------
 # Step 5: placement (old-to-new token map + page table)
 # --------------------------------------------------------------------------

@@ -109,7 +109,7 @@ def test_write_then_restore_cycle(torch):
     layout = oracle.block_layout(req.tags, s.block_tokens, s.num_kv_heads, s.head_dim)
     for b in oracle.reused_blocks(req):
         slots, kk, vv = oracle.restore_block(ref_p, ref_s, s, req, 0, b, layout)  # oracle reads its own checkpoint
-        st.add(kh[0, slots], kk, s.out_dtype)
+        st.add(kh[0, slots], kk, s.out_dtype, int(req.delta))
         st.add(vh[0, slots], vv, s.out_dtype)
     st.assert_ok(s.out_dtype)
     log(f"  cycle: {st}")

@@ -150,6 +150,80 @@ def test_rounding_is_single_not_double():
 
 
 # ---------------------------------------------------------------------------
+# Accepted results: exactly rounded, or the other neighbour of a near-tie.
+# ---------------------------------------------------------------------------
+
+def test_near_tie_classification_hand_cases():
+    bf = oracle.OUT_BF16
+    # (exact, got bits, slack, expected class): 0 exact, 1 near-tie, 2 wrong.
+    cases = [
+        (1 + 2.0 ** -8, 0x3F80, None, 0),                  # a tie, rounded to even
+        (1 + 2.0 ** -8, 0x3F81, None, 1),                  # its other neighbour
+        (1 + 2.0 ** -8 + 2.0 ** -30, 0x3F80, None, 1),     # 2^-30 above the midpoint: inside 2^-23 |x|
+        (1 + 2.0 ** -8 - 2.0 ** -30, 0x3F81, None, 1),
+        (1 + 2.0 ** -8 + 2.0 ** -20, 0x3F80, None, 2),     # 2^-20 above: only 0x3F81 is correct
+        (1 + 2.0 ** -8 + 2.0 ** -20, 0x3F81, None, 0),
+        (1 + 2.0 ** -8, 0x3F82, None, 2),                  # two steps away
+        (-(1 + 2.0 ** -8), 0xBF81, None, 1),               # negative tie
+        (1.0 + 2.0 ** -7, 0x3F80, None, 2),                # a representable value, one step off
+        (0.0, 0x8000, None, 2),                            # signed zero must match ...
+        (0.0, 0x8000, np.float64(1e-30), 1),               # ... except for rotated keys
+        (2.0 ** -9, 0x3B00, None, 0),
+        (3 * 2.0 ** -9, 0x3BC0, None, 0),                  # 1.5 * 2^-8: bf16 has it exactly
+    ]
+    for x, g, slack, cls in cases:
+        same, near = oracle.classify_outputs(np.array([g], np.uint16), np.array([x]), bf, slack)
+        assert (0 if same[0] else 1 if near[0] else 2) == cls, (x, hex(g))
+    # binary16: the midpoint between 1 and 1 + 2^-10
+    hf = oracle.OUT_FP16
+    for x, g, cls in ((1 + 2.0 ** -11, 0x3C00, 0), (1 + 2.0 ** -11, 0x3C01, 1),
+                      (1 + 2.0 ** -11 + 2.0 ** -16, 0x3C00, 2), (1 + 2.0 ** -11 + 2.0 ** -40, 0x3C00, 1)):
+        same, near = oracle.classify_outputs(np.array([g], np.uint16), np.array([x]), hf)
+        assert (0 if same[0] else 1 if near[0] else 2) == cls, (x, hex(g))
+
+
+@pytest.mark.parametrize("out_dtype", [oracle.OUT_FP16, oracle.OUT_BF16])
+def test_double_rounding_through_float32_is_accepted_and_truncation_is_not(out_dtype):
+    """Rounding through numpy's float32 first (what the kernel does) always
+    lands on an accepted result; a truncating conversion, a systematic 1-ulp
+    error, is caught on a large share of elements."""
+    rng = np.random.default_rng(17)
+    x = np.concatenate([rng.standard_normal(200000), rng.standard_normal(20000) * 1e-3])
+    # values built to sit within 2^-30 of a midpoint of the output format
+    kept = 8 if out_dtype == oracle.OUT_BF16 else 11
+    m, e = np.frexp(rng.standard_normal(20000))
+    mids = np.ldexp(np.floor(np.ldexp(m, kept)) + 0.5, e - kept)
+    x = np.concatenate([x, mids * (1 + rng.uniform(-2.0 ** -30, 2.0 ** -30, mids.size))])
+    f32 = x.astype(np.float32).astype(np.float64)
+    twice = oracle.round_to_output(f32, out_dtype)
+    same, near = oracle.classify_outputs(twice, x, out_dtype)
+    assert (same | near).all()
+    assert near.sum() > 100  # the built near-ties do misround
+    # truncation toward zero: wrong wherever it differs from the exact rounding
+    # (the random values; the built near-ties are excluded)
+    x = x[:220000]
+    want = oracle.round_to_output(x, out_dtype)
+    vals = oracle.output_values(want, out_dtype)
+    trunc = np.where(np.abs(vals) > np.abs(x), want - 1, want).astype(np.uint16)  # one step toward zero
+    same, near = oracle.classify_outputs(trunc, x, out_dtype)
+    moved = trunc != want
+    assert (~(same | near))[moved].mean() > 0.99
+
+
+def test_rotation_slack_bound():
+    """The slack covers a rotation through a differently rounded angle: the
+    same keys rotated with angles perturbed by 4 ulp stay within it."""
+    rng = np.random.default_rng(23)
+    k = rng.standard_normal((256, 4, 128)) * np.where(rng.random((1, 4, 128)) < 0.02, 8.0, 1.0)
+    for delta in (1, -1500, 4096, 20000):
+        f = oracle.rope_frequencies(5e5, 128)
+        a = oracle.rotate(k, delta * f)
+        b = oracle.rotate(k, delta * f * (1 + 4 * 2.0 ** -52))
+        assert (np.abs(a - b) <= oracle.rotation_slack(a, delta) / 4).all()
+    assert oracle.rotation_slack(k, 0) is None
+
+
+# ---------------------------------------------------------------------------
 # RoPE correction (Eq. 3)
 # ---------------------------------------------------------------------------
 

@@ -45,7 +45,14 @@ WORKLOAD_TEXT = {
     "llama70b": "Llama-70B-shaped: 80 layers x 8 KV heads x head_dim 128, 65536-token suffix, block 64, page 32, "
                 "bf16 cache, 60/30/10 tag mix, 12% repair, delta +4096",
     "tiny": "tiny: 1 layer x 2 KV heads x head_dim 64, 512 tokens, block 16",
+    "batched16": "batched resumes: 16 requests on the 32-layer 8B shape, suffixes of 4096-65536 tokens, "
+                 "per-request delta in [-8192, 8192] and Dirichlet tag mixes, 5-20% repair, one 2^20-slot paged pool "
+                 "with interleaved page ownership",
 }
+# Workloads whose old caches of all layers do not fit beside the pool and the
+# checkpoint: their checkpoint is written layer by layer (not timed), and one
+# buffer set is used.
+LAYERWISE = {"batched16"}
 
 
 KV_LAYOUT_TEXT = {
@@ -81,9 +88,6 @@ def measured_traffic(workload: str, int4: str, layout: str, kernel: str = "resto
 # CPU baseline: the oracle, per layer, in worker processes
 # ---------------------------------------------------------------------------
 
-_CPU_CASE = None
-
-
 def _oracle_layer(args):
     """One layer of one request: the oracle writes its checkpoint from the
     drawn rows (timed separately), then restores it (timed)."""
@@ -94,8 +98,7 @@ def _oracle_layer(args):
     import oracle
     from oracle import quantize as oq
 
-    ri, layer = args
-    case = _CPU_CASE
+    case, ri, layer = args
     req = case.requests[ri]
     _, kb, vb = case.suffix_bits(ri, layer)
     t = time.perf_counter()
@@ -119,27 +122,20 @@ def _oracle_layer(args):
     return time.perf_counter() - t, t_write
 
 
-def cpu_baseline(case, max_workers: int = 16, target_layers: int = 32):
-    """Oracle throughput on the host cores over a bounded sample of layers."""
-    global _CPU_CASE
-    _CPU_CASE = case
-    try:
-        n_cpu = len(os.sched_getaffinity(0))
-    except AttributeError:
-        n_cpu = os.cpu_count() or 1
-    workers = max(1, min(max_workers, n_cpu))
+def cpu_baseline(case, pool, workers: int, target_layers: int = 32):
+    """Oracle throughput on the host cores over a bounded sample of layers,
+    one layer per job on ``pool`` (``workers`` processes, forked before the
+    benchmark touched the GPU)."""
     layers = list(range(min(case.shape.num_layers, max(target_layers, workers))))
-    jobs = [(0, l) for l in layers]
-    ctx = mp.get_context("fork")
-    with ctx.Pool(workers) as pool:
-        per_layer = pool.map(_oracle_layer, jobs)
+    jobs = [(case, 0, l) for l in layers]
+    per_layer = pool.map(_oracle_layer, jobs) if pool is not None else [_oracle_layer(j) for j in jobs]
     # Each process times its own layer; the pool runs `workers` layers at once.
     restore_cpu = sum(t for t, _ in per_layer)
     write_cpu = sum(t for _, t in per_layer)
     rounds = -(-len(layers) // workers)
     wall = restore_cpu / len(layers) * rounds
     # One layer in this process alone: the single-worker rate, free of the pool's memory contention.
-    one_layer_s, _ = _oracle_layer((0, 0))
+    one_layer_s, _ = _oracle_layer((case, 0, 0))
     per_layer_bytes = case.algorithmic_bytes()["total"] / case.shape.num_layers
     sample_bytes = per_layer_bytes * len(layers)
     return {
@@ -179,7 +175,6 @@ def oracle_configs(max_workers: int = 16, sampled_layers: int = 4) -> dict:
     estimate assumes the jobs spread evenly over the workers."""
     from paper_2609_26219_amd import workloads as wl
 
-    global _CPU_CASE
     try:
         n_cpu = len(os.sched_getaffinity(0))
     except AttributeError:
@@ -192,11 +187,14 @@ def oracle_configs(max_workers: int = 16, sampled_layers: int = 4) -> dict:
         layers = list(range(L)) if L <= 32 else list(range(sampled_layers))
         if name == "batched16":
             layers = list(range(sampled_layers))
-        jobs = [(ri, l) for ri in range(len(case.requests)) for l in layers]
-        _CPU_CASE = case
+        jobs = [(case, ri, l) for ri in range(len(case.requests)) for l in layers]
         t = time.perf_counter()
-        with mp.get_context("fork").Pool(min(workers, len(jobs))) as pool:
+        pool = mp.get_context("fork").Pool(min(workers, len(jobs)))  # this mode never touches the GPU
+        try:
             times = pool.map(_oracle_layer, jobs)
+        finally:
+            pool.close()
+            pool.join()
         wall_measured = time.perf_counter() - t
         restore_cpu = sum(r for r, _ in times)
         full_cpu = restore_cpu * L / len(layers)
@@ -216,7 +214,6 @@ def oracle_configs(max_workers: int = 16, sampled_layers: int = 4) -> dict:
         }
         log(f"[bench] oracle {name}: {out[name]['est_wall_s']} s per restore at {workers} workers"
             f"{' (extrapolated)' if len(layers) < L else ''}, {out[name]['GBps']} GB/s")
-    _CPU_CASE = None
     return out
 
 
@@ -614,6 +611,20 @@ def main():
               f"(the restore shards by request, layer or KV head with no exchange step).", file=sys.stderr)
         sys.exit(2)
 
+    # Worker processes (row draws, the CPU oracle) are forked now, before
+    # anything touches the GPU, and joined at the end.
+    from paper_2609_26219_amd import device
+    from paper_2609_26219_amd import workloads as wl
+
+    n_workers = wl.default_workers()
+    pool = device.start_workers(n_workers)
+    try:
+        run(args, pool, n_workers)
+    finally:
+        device.stop_workers()
+
+
+def run(args, pool, n_workers):
     import torch
 
     from paper_2609_26219_amd import binding
@@ -629,22 +640,48 @@ def main():
     case = wl.make_case(args.workload, int4_tag=int4_tag)
     layout = wl.KV_PAIRED if args.kv_layout == "paired" else wl.KV_SEPARATE
     case.shape = dataclasses.replace(case.shape, kv_layout=layout)
-    old = OldCaches(case)
-    log(f"[bench] drew {args.workload} old caches in {time.perf_counter() - t:.1f} s")
     stream = torch.cuda.current_stream()
-
-    # Checkpoint write (offload side): every layer, every block, one launch.
-    ck = DeviceCheckpoint(case, old)
-    w_info = ck.info
-    w_bytes = w_info["bytes_read"] + w_info["bytes_written"]
-    w_ms, _ = time_launches(torch, lambda i: ck.write(stream), args.write_steps, 2, stream)
-    w_avg = sum(w_ms) / len(w_ms)
-    w_achieved = w_bytes / (w_avg * 1e-3) / 1e9
-    log(f"[bench] checkpoint write avg {w_avg * 1e3:.1f} us, {w_achieved:.0f} GB/s")
-    ck.old = None
-
-    sets = [DeviceRestore(case, checkpoint=(ck.payload, ck.scales)) for _ in range(max(1, args.sets))]
-    del ck
+    layerwise = args.workload in LAYERWISE
+    if layerwise:
+        args.sets, args.host_steps = 1, 0
+        args.no_representations = args.no_other_layout = True
+        old = None
+        sets = [DeviceRestore(case)]
+        log(f"[bench] wrote the {args.workload} checkpoint layer by layer in {time.perf_counter() - t:.1f} s")
+        checkpoint_write = None
+    else:
+        old = OldCaches(case)
+        log(f"[bench] drew {args.workload} old caches in {time.perf_counter() - t:.1f} s")
+        # Checkpoint write (offload side): every layer, every block, one launch.
+        ck = DeviceCheckpoint(case, old)
+        w_info = ck.info
+        w_bytes = w_info["bytes_read"] + w_info["bytes_written"]
+        w_ms, _ = time_launches(torch, lambda i: ck.write(stream), args.write_steps, 2, stream)
+        w_avg = sum(w_ms) / len(w_ms)
+        w_achieved = w_bytes / (w_avg * 1e-3) / 1e9
+        log(f"[bench] checkpoint write avg {w_avg * 1e3:.1f} us, {w_achieved:.0f} GB/s")
+        checkpoint_write = {
+            "what": "pkv_quantize_gather of every block of every layer from the old paged caches "
+                    "(the offload side that produces the restored checkpoint), one launch",
+            "us": round(w_avg * 1e3, 1),
+            "us_p10_p50_p90": [round(w_ms[int(q * (len(w_ms) - 1))] * 1e3, 1) for q in (0.1, 0.5, 0.9)],
+            "launches": len(w_ms),
+            "algorithmic_bytes": w_bytes,
+            "bytes_read": w_info["bytes_read"],
+            "bytes_written": w_info["bytes_written"],
+            "roofline": {
+                "bound": "hbm",
+                "achieved": round(w_achieved, 1),
+                "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s",
+                "frac": round(w_achieved / HBM_PEAK_GBPS, 4),
+                "traffic": measured_traffic(args.workload, args.int4, args.kv_layout, "gather_tile_kernel",
+                                            GATHER_SRC),
+            },
+        }
+        ck.old = None
+        sets = [DeviceRestore(case, checkpoint=(ck.payload, ck.scales)) for _ in range(max(1, args.sets))]
+        del ck
     torch.cuda.empty_cache()
     info = sets[0].info
     nbytes = info["bytes_read"] + info["bytes_written"]
@@ -698,25 +735,9 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": measured_traffic(args.workload, args.int4, args.kv_layout),
         },
-        "checkpoint_write": {
-            "what": "pkv_quantize_gather of every block of every layer from the old paged caches "
-                    "(the offload side that produces the restored checkpoint), one launch",
-            "us": round(w_avg * 1e3, 1),
-            "us_p10_p50_p90": [round(w_ms[int(q * (len(w_ms) - 1))] * 1e3, 1) for q in (0.1, 0.5, 0.9)],
-            "launches": len(w_ms),
-            "algorithmic_bytes": w_bytes,
-            "bytes_read": w_info["bytes_read"],
-            "bytes_written": w_info["bytes_written"],
-            "roofline": {
-                "bound": "hbm",
-                "achieved": round(w_achieved, 1),
-                "peak": HBM_PEAK_GBPS,
-                "unit": "GB/s",
-                "frac": round(w_achieved / HBM_PEAK_GBPS, 4),
-                "traffic": measured_traffic(args.workload, args.int4, args.kv_layout, "gather_tile_kernel",
-                                            GATHER_SRC),
-            },
-        },
+        "checkpoint_write": checkpoint_write if checkpoint_write is not None else
+        "not timed: this workload's old caches of all layers do not fit beside its pool, so its checkpoint is "
+        "written layer by layer",
     }
     parity = None
     if not args.no_cpu_baseline:
@@ -747,7 +768,7 @@ def main():
         out["copy_ref_GBps"] = copy_reference(torch)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
-        out["cpu_baseline"] = cpu_baseline(case)
+        out["cpu_baseline"] = cpu_baseline(case, pool, n_workers)
         out["cpu_baseline"]["oracle_parity"] = parity
     print(json.dumps(out), flush=True)
 

@@ -44,13 +44,15 @@
  *    owned by nobody keep their bytes.
  *
  * Arithmetic: decode exact; keys rotated in double precision with a
- * double-precision cos/sin(Delta * theta_i) table (theta_i =
- * rope_theta^(-2i/D), rotate-half pairs (i, i + D/2)); values decoded in
- * single precision; one round-to-nearest-even to the output dtype after an
- * intermediate single-precision value.  Every element is within one unit in
- * the last place of the exactly rounded result.  When Delta == 0 keys are
- * not rotated at all (R(0) = I), so the FP16 tag with Delta == 0 and fp16
- * output is a bit-exact copy.
+ * double-precision cos/sin(Delta * f_i) table over the model's rotary pairs
+ * and frequencies f_i (pkv_rope_style_t, rotary_dim and inv_freq in
+ * pkv_model_t); values decoded in single precision; one round-to-nearest-even
+ * to the output dtype after an intermediate single-precision value.  So every
+ * element is the exactly rounded result, except within the double-rounding
+ * window of a rounding midpoint (about 2^-24 relative), where it may be the
+ * midpoint's other neighbour.  When Delta == 0 keys are not rotated at all
+ * (R(0) = I), so the FP16 tag with Delta == 0 and fp16 output is a bit-exact
+ * copy.
  * ----------------------------------------------------------------------------
  */
 #ifndef PKV_H
@@ -261,8 +263,7 @@ typedef struct {
 } pkv_checkpoint_request_t;
 
 /* Validate a checkpoint write and build its plan on the current HIP device
- * (same model constraints as pkv_restore_plan, plus num_kv_heads * head_dim
- * / 16 * ceil(block_tokens / 4) <= 1024).  Every row of every block must sit
+ * (same model constraints as pkv_restore_plan).  Every row of every block must sit
  * on a mapped, in-range page (PKV_ERR_PAGE_UNMAPPED / _OUT_OF_RANGE);
  * overlapping payload or scale ranges of two requests are
  * PKV_ERR_INVALID_ARGUMENT.  Host arrays are copied.  Errors: as
@@ -271,10 +272,16 @@ pkv_status_t pkv_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoint_
                                  int32_t num_requests, pkv_plan_t** out);
 
 /* Enqueue the checkpoint write of a pkv_checkpoint_plan on `hip_stream`.
- *   k_cache / v_cache : device, read only, 16-byte aligned, cache_bytes as in
- *                       pkv_restore for the model's kv_layout;
- *   payload / scales  : device outputs, >= the plan's payload_bytes / scale_bytes,
- *                       16- / 8-byte aligned, not overlapping each other or the caches.
+ *   k_cache / v_cache : device memory of the plan's device, read only, 16-byte
+ *                       aligned, cache_bytes as in pkv_restore for the model's kv_layout;
+ *   payload / scales  : outputs, >= the plan's payload_bytes / scale_bytes,
+ *                       16- / 8-byte aligned, not overlapping each other or the
+ *                       caches: device memory of the plan's device, or pinned
+ *                       host memory (hipHostMalloc), which the kernel writes
+ *                       over the host link (the checkpoint lands in CPU DRAM,
+ *                       where the paper keeps it, with no staging copy).
+ * Pageable host memory or another device's memory, for any buffer, is
+ * PKV_ERR_INVALID_ARGUMENT, and nothing is written.
  * Only bytes inside the requests' checkpoint ranges are written.
  * A restore plan passed here (or a checkpoint plan passed to pkv_restore) is
  * PKV_ERR_INVALID_ARGUMENT.  Errors: PKV_ERR_INVALID_ARGUMENT, PKV_ERR_DEVICE.
@@ -324,6 +331,14 @@ typedef struct {
 } pkv_plan_info_t;
 
 pkv_status_t pkv_plan_query(const pkv_plan_t* plan, pkv_plan_info_t* info);
+
+/* Bytes of request `req`'s checkpoint payload, all layers (the clustered
+ * layout above, repair blocks included), for a restore or a checkpoint plan:
+ * the payload that Section IV-D's quantize-and-gather writes and its
+ * transport stage draws F blocks from (Eq. 12), and the per-representation
+ * checkpoint size of Section V-D.  Host only.  Errors:
+ * PKV_ERR_INVALID_ARGUMENT (NULL plan or bytes, req outside [0, num_requests)). */
+pkv_status_t pkv_plan_payload_bytes(const pkv_plan_t* plan, int32_t req, uint64_t* bytes);
 
 /* Static description of a status code. */
 const char* pkv_status_string(pkv_status_t status);

@@ -25,7 +25,8 @@ PKV_ERR_DEVICE = -7
 
 # Every symbol include/pkv.h declares.
 EXPORTED = ("pkv_payload_size", "pkv_restore_plan", "pkv_restore", "pkv_restore_from_host", "pkv_free",
-            "pkv_plan_query", "pkv_status_string", "pkv_checkpoint_plan", "pkv_quantize_gather", "pkv_plan_repair")
+            "pkv_plan_query", "pkv_status_string", "pkv_checkpoint_plan", "pkv_quantize_gather", "pkv_plan_repair",
+            "pkv_plan_payload_bytes")
 
 
 class PkvModel(ctypes.Structure):
@@ -97,6 +98,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pkv_quantize_gather.restype = i32
     lib.pkv_plan_repair.argtypes = [i32, i32, ctypes.c_int64, vp, ctypes.c_double, vp, ctypes.POINTER(ctypes.c_int64)]
     lib.pkv_plan_repair.restype = i32
+    lib.pkv_plan_payload_bytes.argtypes = [vp, i32, ctypes.POINTER(u64)]
+    lib.pkv_plan_payload_bytes.restype = i32
     _lib = lib
     return lib
 
@@ -282,6 +285,19 @@ def pkv_plan_query(plan: Plan) -> dict:
     if st != PKV_OK:
         raise PkvError(st, "pkv_plan_query")
     return {name: getattr(info, name) for name, _ in PkvPlanInfo._fields_}
+
+
+def pkv_plan_payload_bytes(plan: Plan, req: int) -> int:
+    """Bytes of request ``req``'s checkpoint payload, all layers."""
+    out = ctypes.c_uint64()
+    st = load().pkv_plan_payload_bytes(plan.handle, int(req), ctypes.byref(out))
+    if st != PKV_OK:
+        raise PkvError(st, "pkv_plan_payload_bytes")
+    return int(out.value)
+
+
+def pkv_plan_payload_bytes_status(plan_handle, req: int, out_ptr) -> int:
+    return load().pkv_plan_payload_bytes(plan_handle, int(req), out_ptr)
 
 
 def pkv_restore(plan: Plan, payload: int, payload_bytes: int, scales: int, scale_bytes: int, k_cache: int,

@@ -610,6 +610,15 @@ pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, co
       return PKV_ERR_INVALID_ARGUMENT;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
+  // The old caches must be device memory of the plan's device; the
+  // checkpoint may also go to pinned host memory, written through its device
+  // mapping.  Anything else would fault in the kernel.
+  const void *p_dev = nullptr, *s_dev = nullptr;
+  pkv_status_t st;
+  if ((st = pkv::device_resident(plan, k_cache)) != PKV_OK || (st = pkv::device_resident(plan, v_cache)) != PKV_OK ||
+      (st = pkv::kernel_accessible(plan, payload, &p_dev)) != PKV_OK ||
+      (st = pkv::kernel_accessible(plan, scales, &s_dev)) != PKV_OK)
+    return st;
 
   const pkv_model_t& m = plan->host.model;
   pkv::GatherArgs a;
@@ -617,8 +626,8 @@ pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, co
   a.page_tables = plan->d_page_tables;
   a.k_cache = static_cast<const uint16_t*>(k_cache);
   a.v_cache = static_cast<const uint16_t*>(v_cache);
-  a.payload = static_cast<uint8_t*>(payload);
-  a.scales = static_cast<uint16_t*>(scales);
+  a.payload = static_cast<uint8_t*>(const_cast<void*>(p_dev));
+  a.scales = static_cast<uint16_t*>(const_cast<void*>(s_dev));
   a.layer_elems = pkv::layer_elems(m);
   a.page_shift = pkv::page_shift(m);
   a.H = m.num_kv_heads;

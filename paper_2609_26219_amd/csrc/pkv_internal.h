@@ -112,6 +112,7 @@ struct HostPlan {
   std::vector<CopyRange> payload_ranges, scale_ranges;
   std::vector<int64_t> payload_layer, scale_layer;
   int64_t rotated_rows = 0;  // restore plans: restored rows whose keys rotate (shift != 0)
+  std::vector<uint64_t> req_payload_bytes;  // per request: bytes of its checkpoint payload, all layers
 };
 
 // Restore workgroups resident per compute unit, chosen per plan: 8 to 16
@@ -201,6 +202,16 @@ struct ByteRange {
 };
 bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache, uint64_t bytes, ByteRange (&ranges)[2],
                   int& count);
+
+// What kind of memory a kernel argument is (hipPointerGetAttributes), so that
+// no launch ever gets a pointer the kernel would fault on.
+//   kernel_accessible: device or managed memory of the plan's device as is,
+//     or pinned host memory through its device mapping (*out receives the
+//     address the kernel uses); pageable host memory or another device's
+//     memory is PKV_ERR_INVALID_ARGUMENT.
+//   device_resident: device or managed memory of the plan's device only.
+pkv_status_t kernel_accessible(const pkv_plan* plan, const void* p, const void** out);
+pkv_status_t device_resident(const pkv_plan* plan, const void* p);
 
 }  // namespace pkv
 

@@ -231,6 +231,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
   if (int64_t(num_requests) * D > std::numeric_limits<int32_t>::max()) return PKV_ERR_INVALID_ARGUMENT;
   try {
     hp.reqs.resize(num_requests);
+    hp.req_payload_bytes.assign(size_t(num_requests), 0);
     hp.tables.resize(size_t(num_requests) * size_t(D));
     // Per request: page table, cos/sin table, block offsets inside a layer.
     std::vector<std::vector<uint64_t>> block_off(num_requests);
@@ -262,6 +263,7 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
             pos += tile_bytes(m, kKeyBits[tag]) + tile_bytes(m, kValueBits[tag]);
           }
       layer_bytes[r] = pos;
+      hp.req_payload_bytes[r] = uint64_t(L) * pos;
       hp.info.payload_bytes = std::max<uint64_t>(hp.info.payload_bytes, q.payload_offset + uint64_t(L) * pos);
       hp.info.scale_bytes =
           std::max<uint64_t>(hp.info.scale_bytes, (q.scale_offset + uint64_t(L) * nb * H * 4) * 2);
@@ -417,6 +419,7 @@ pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoin
   hp.info.kind = 1;
   hp.info.cache_bytes = cache_bytes(m);
   try {
+    hp.req_payload_bytes.assign(size_t(num_requests), 0);
     for (int32_t r = 0; r < num_requests; ++r) {
       const pkv_checkpoint_request_t& q = requests[r];
       const int64_t nb = ceil_div(q.suffix_tokens, B);
@@ -432,6 +435,7 @@ pkv_status_t build_checkpoint_plan(const pkv_model_t* model, const pkv_checkpoin
             pos += tile_bytes(m, kKeyBits[tag]) + tile_bytes(m, kValueBits[tag]);
           }
       const uint64_t layer_bytes = pos;
+      hp.req_payload_bytes[r] = uint64_t(L) * layer_bytes;
       hp.info.payload_bytes = std::max<uint64_t>(hp.info.payload_bytes, q.payload_offset + uint64_t(L) * layer_bytes);
       hp.info.scale_bytes = std::max<uint64_t>(hp.info.scale_bytes, (q.scale_offset + uint64_t(L) * nb * H * 4) * 2);
       for (int64_t l = 0; l < L; ++l) {

@@ -474,11 +474,11 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   return PKV_OK;
 }
 
-// Where the kernel may read an input from: device or managed memory of the
+// Where a kernel may read or write a buffer: device or managed memory of the
 // plan's device as is; pinned host memory through its device mapping (the
-// kernel then reads it over the host link).  Pageable host memory, or memory
-// of another device, is rejected: the kernel would fault on it.
-pkv_status_t kernel_readable(const pkv_plan* plan, const void* p, const void** out) {
+// kernel then reaches it over the host link).  Pageable host memory, or
+// memory of another device, is rejected: the kernel would fault on it.
+pkv_status_t kernel_accessible(const pkv_plan* plan, const void* p, const void** out) {
   hipPointerAttribute_t a;
   if (hipPointerGetAttributes(&a, p) != hipSuccess) {
     (void)hipGetLastError();
@@ -496,7 +496,7 @@ pkv_status_t kernel_readable(const pkv_plan* plan, const void* p, const void** o
 }
 
 // Caches must be device (or managed) memory of the plan's device.
-pkv_status_t device_writable(const pkv_plan* plan, const void* p) {
+pkv_status_t device_resident(const pkv_plan* plan, const void* p) {
   hipPointerAttribute_t a;
   if (hipPointerGetAttributes(&a, p) != hipSuccess) {
     (void)hipGetLastError();
@@ -584,9 +584,9 @@ pkv_status_t pkv_restore(const pkv_plan_t* plan, const void* payload, uint64_t p
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
   const void *p_dev = nullptr, *s_dev = nullptr;
-  if ((st = pkv::kernel_readable(plan, payload, &p_dev)) != PKV_OK ||
-      (st = pkv::kernel_readable(plan, scales, &s_dev)) != PKV_OK || (st = pkv::device_writable(plan, k_cache)) != PKV_OK ||
-      (st = pkv::device_writable(plan, v_cache)) != PKV_OK)
+  if ((st = pkv::kernel_accessible(plan, payload, &p_dev)) != PKV_OK ||
+      (st = pkv::kernel_accessible(plan, scales, &s_dev)) != PKV_OK || (st = pkv::device_resident(plan, k_cache)) != PKV_OK ||
+      (st = pkv::device_resident(plan, v_cache)) != PKV_OK)
     return st;
   return pkv::launch_restore(plan, p_dev, s_dev, k_cache, v_cache, 0, info.num_units,
                              static_cast<hipStream_t>(hip_stream));
@@ -606,8 +606,8 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
     return PKV_ERR_INVALID_ARGUMENT;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
-  if ((st = pkv::device_writable(plan, payload)) != PKV_OK || (st = pkv::device_writable(plan, scales)) != PKV_OK ||
-      (st = pkv::device_writable(plan, k_cache)) != PKV_OK || (st = pkv::device_writable(plan, v_cache)) != PKV_OK)
+  if ((st = pkv::device_resident(plan, payload)) != PKV_OK || (st = pkv::device_resident(plan, scales)) != PKV_OK ||
+      (st = pkv::device_resident(plan, k_cache)) != PKV_OK || (st = pkv::device_resident(plan, v_cache)) != PKV_OK)
     return st;
   pkv_plan* p = const_cast<pkv_plan*>(plan);  // the copy streams and events are created on first use
   const int64_t L = plan->host.model.num_layers;
@@ -695,6 +695,12 @@ void pkv_free(pkv_plan_t* plan) {
     if (switched) (void)hipSetDevice(cur);
   }
   delete plan;
+}
+
+pkv_status_t pkv_plan_payload_bytes(const pkv_plan_t* plan, int32_t req, uint64_t* bytes) {
+  if (!plan || !bytes || req < 0 || size_t(req) >= plan->host.req_payload_bytes.size()) return PKV_ERR_INVALID_ARGUMENT;
+  *bytes = plan->host.req_payload_bytes[size_t(req)];
+  return PKV_OK;
 }
 
 pkv_status_t pkv_plan_query(const pkv_plan_t* plan, pkv_plan_info_t* info) {

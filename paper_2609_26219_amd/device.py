@@ -13,8 +13,10 @@ No step of the method's arithmetic happens here.
 """
 from __future__ import annotations
 
+import atexit
 import dataclasses
 import multiprocessing as mp
+import sys
 from typing import Dict, Iterator, Optional, Sequence, Tuple
 
 import numpy as np
@@ -30,31 +32,65 @@ def _to_int16(t):
     return torch.where(t >= 32768, t - 65536, t).to(torch.int16)
 
 
-_DRAW_CASE = None
+# Worker processes that draw suffix rows (numpy only).  They are forked by
+# start_workers() before the process first touches the GPU, so no worker
+# inherits GPU state, and closed and joined by stop_workers() (also at exit).
+_POOL = None
 
 
-def _draw_job(key):
-    ri, layer = key
-    return key, _DRAW_CASE.suffix_bits(ri, layer)
+def start_workers(workers: Optional[int] = None):
+    """Fork the draw workers now (call before any GPU work); returns the pool,
+    or None for one worker."""
+    global _POOL
+    n = workers or wl.default_workers()
+    if _POOL is None and n > 1:
+        _POOL = mp.get_context("fork").Pool(n)
+        atexit.register(stop_workers)
+    return _POOL
+
+
+def stop_workers() -> None:
+    global _POOL
+    if _POOL is not None:
+        pool, _POOL = _POOL, None
+        pool.close()
+        pool.join()
+
+
+def worker_pool():
+    """The pool of :func:`start_workers`, or None."""
+    return _POOL
+
+
+def _gpu_initialised() -> bool:
+    torch = sys.modules.get("torch")
+    return torch is not None and torch.cuda.is_initialized()
+
+
+def _draw_job(args):
+    case, key = args
+    return key, case.suffix_bits(*key)
 
 
 def suffix_rows(case: wl.Case, layers: Sequence[int], workers: Optional[int] = None
                 ) -> Iterator[Tuple[int, int, Tuple[np.ndarray, np.ndarray, np.ndarray]]]:
     """Yield (request, layer, (old slots, K bits, V bits)) for every layer in
     ``layers`` (layer-major) and every request.  Each distinct draw is made
-    once, in worker processes, and dropped after its last use."""
-    global _DRAW_CASE
+    once and dropped after its last use: in the workers of
+    :func:`start_workers` if they run; else, before the GPU is touched, in a
+    pool forked for this call; else (``workers`` 1, or the GPU already in
+    use, where forking is not safe) in this process."""
     order = [(ri, layer) for layer in layers for ri in range(len(case.requests))]
     keys = list(dict.fromkeys((ri, case.source_layer(l)) for ri, l in order))
     last_use = {(ri, case.source_layer(l)): i for i, (ri, l) in enumerate(order)}
     workers = min(workers or wl.default_workers(), len(keys))
-    pool = None
+    pool, own = None, False
     if workers > 1:
-        _DRAW_CASE = case
-        pool = mp.get_context("fork").Pool(workers)
-        results = pool.imap(_draw_job, keys)
-    else:
-        results = ((k, case.suffix_bits(*k)) for k in keys)
+        pool = _POOL
+        if pool is None and not _gpu_initialised():
+            pool, own = mp.get_context("fork").Pool(workers), True
+    results = pool.imap(_draw_job, [(case, k) for k in keys]) if pool is not None else \
+        ((k, case.suffix_bits(*k)) for k in keys)
     try:
         drawn: Dict[Tuple[int, int], Tuple[np.ndarray, np.ndarray, np.ndarray]] = {}
         for i, (ri, layer) in enumerate(order):
@@ -67,7 +103,7 @@ def suffix_rows(case: wl.Case, layers: Sequence[int], workers: Optional[int] = N
                 del drawn[key]
             yield ri, layer, val
     finally:
-        if pool is not None:
+        if own:
             pool.terminate()
             pool.join()
 

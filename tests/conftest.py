@@ -16,3 +16,10 @@ def pytest_configure(config):
 @pytest.fixture(scope="session")
 def repo_root():
     return ROOT
+
+
+def pytest_collection_finish(session):
+    """GPU runs: fork the suffix-row draw workers before any test touches the GPU."""
+    if any(item.get_closest_marker("gpu") for item in session.items):
+        from paper_2609_26219_amd import device
+        device.start_workers()

@@ -53,6 +53,13 @@ def test_library_exports_every_declared_symbol(lib):
         assert hasattr(lib, name)
 
 
+def test_plan_payload_bytes_rejects_null(lib):
+    import ctypes
+    out = ctypes.c_uint64(5)
+    assert pb.pkv_plan_payload_bytes_status(None, 0, ctypes.byref(out)) == pb.PKV_ERR_INVALID_ARGUMENT
+    assert out.value == 5
+
+
 def test_status_strings(lib):
     for code in range(-7, 1):
         assert pb.pkv_status_string(code) != "unknown status"

@@ -268,3 +268,22 @@ def test_llama70b_full_size(torch):
 def test_batched16_full_size(torch):
     log("[gpu] batched16: 16 requests on a 2^20-slot pool, 4 sampled (request, layer) + untouched check")
     _full_size(wl.make_case("batched16", distinct_layers=1), [(0, 0), (5, 13), (11, 31), (15, 7)], torch)
+
+
+def test_plan_payload_bytes_per_request(torch):
+    """pkv_plan_payload_bytes: each request's checkpoint size, for restore and
+    checkpoint plans alike, equal to the oracle's layout walk; requests
+    outside the plan are argument errors."""
+    import ctypes
+
+    case = wl.make_custom(21, L=2, H=3, D=32, B=8, P=4, n_tokens=(37, 5, 16), deltas=(3, 0, -2),
+                          rho0s=(9, 4, 30), tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1))
+    plans = (pb.pkv_restore_plan(case.shape, case.requests), pb.pkv_checkpoint_plan(case.src_shape, case.requests))
+    for plan in plans:
+        for ri, req in enumerate(case.requests):
+            assert pb.pkv_plan_payload_bytes(plan, ri) == oracle.request_payload_bytes(case.shape, req)
+        out = ctypes.c_uint64(7)
+        for bad in (-1, len(case.requests)):
+            assert pb.pkv_plan_payload_bytes_status(plan.handle, bad, ctypes.byref(out)) == pb.PKV_ERR_INVALID_ARGUMENT
+        assert pb.pkv_plan_payload_bytes_status(plan.handle, 0, None) == pb.PKV_ERR_INVALID_ARGUMENT
+        assert out.value == 7

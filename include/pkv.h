@@ -228,6 +228,34 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
                                    uint64_t payload_bytes, void* scales, uint64_t scale_bytes, void* k_cache,
                                    void* v_cache, uint64_t cache_bytes, void* hip_stream);
 
+/* The streamed restore of pkv_restore_from_host for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): no device checkpoint buffers are passed,
+ * and the call allocates nothing.  The checkpoint is staged through a buffer
+ * of the library, a static device array of 64 MiB (payload windows) + 4 MiB
+ * (scales) that each GPU the library runs on holds until the process ends.
+ * For each layer and request in turn, on `hip_stream` only: the request's
+ * layer scales are copied into the stage, then the request's reused blocks
+ * (payload order) go through in windows of at most 64 MiB, each copied from
+ * host memory (blocks closer than 512 KiB merged into one copy) and restored
+ * before the next window's copies start.  One DMA stream carries every copy,
+ * so the host link runs below the two-stream rate of pkv_restore_from_host.
+ *   host_payload / host_scales : pinned host memory (hipHostMalloc) holding
+ *     the whole checkpoint (>= the plan's payload_bytes / scale_bytes);
+ *     pageable memory is PKV_ERR_INVALID_ARGUMENT;
+ *   k_cache, v_cache, cache_bytes, hip_stream : as in pkv_restore.
+ * Limit: one request-layer's scales, ceil(N / B) * H * 8 bytes, must fit in
+ * 4 MiB (PKV_ERR_INVALID_ARGUMENT otherwise, before anything is enqueued);
+ * every block fits a window.  Every call on one GPU shares that GPU's stage
+ * and leaves the last window in it (nothing in it needs to start at zero):
+ * calls that overlap on one GPU -- on different streams, or from several
+ * threads -- race and must be ordered by the caller.  Returns after
+ * enqueueing.  Errors: PKV_ERR_INVALID_ARGUMENT, PKV_ERR_DEVICE. */
+pkv_status_t pkv_restore_from_host_noalloc(const pkv_plan_t* plan, const void* host_payload,
+                                           uint64_t host_payload_bytes, const void* host_scales,
+                                           uint64_t host_scale_bytes, void* k_cache, void* v_cache,
+                                           uint64_t cache_bytes, void* hip_stream);
+
 /* Release a plan and its device memory.  NULL is a no-op.  The caller must
  * make sure no enqueued restore still uses it. */
 void pkv_free(pkv_plan_t* plan);

@@ -26,7 +26,7 @@ PKV_ERR_DEVICE = -7
 # Every symbol include/pkv.h declares.
 EXPORTED = ("pkv_payload_size", "pkv_restore_plan", "pkv_restore", "pkv_restore_from_host", "pkv_free",
             "pkv_plan_query", "pkv_status_string", "pkv_checkpoint_plan", "pkv_quantize_gather", "pkv_plan_repair",
-            "pkv_plan_payload_bytes")
+            "pkv_plan_payload_bytes", "pkv_restore_from_host_noalloc")
 
 
 class PkvModel(ctypes.Structure):
@@ -98,6 +98,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pkv_quantize_gather.restype = i32
     lib.pkv_plan_repair.argtypes = [i32, i32, ctypes.c_int64, vp, ctypes.c_double, vp, ctypes.POINTER(ctypes.c_int64)]
     lib.pkv_plan_repair.restype = i32
+    lib.pkv_restore_from_host_noalloc.argtypes = [vp, vp, u64, vp, u64, vp, vp, u64, vp]
+    lib.pkv_restore_from_host_noalloc.restype = i32
     lib.pkv_plan_payload_bytes.argtypes = [vp, i32, ctypes.POINTER(u64)]
     lib.pkv_plan_payload_bytes.restype = i32
     _lib = lib
@@ -340,6 +342,34 @@ def restore_from_host_tensors(plan: Plan, host_payload, host_scales, payload, sc
                           nbytes(host_scales), payload.data_ptr(), nbytes(payload), scales.data_ptr(),
                           nbytes(scales), k_cache.data_ptr(), v_cache.data_ptr(), cache_nbytes(k_cache, v_cache),
                           stream.cuda_stream)
+
+
+def pkv_restore_from_host_noalloc(plan: Plan, host_payload: int, host_payload_bytes: int, host_scales: int,
+                                  host_scale_bytes: int, k_cache: int, v_cache: int, cache_bytes: int,
+                                  stream: int = 0) -> None:
+    """Enqueue the allocation-free streamed restore; host_* are pinned host addresses."""
+    st = pkv_restore_from_host_noalloc_status(plan, host_payload, host_payload_bytes, host_scales, host_scale_bytes,
+                                              k_cache, v_cache, cache_bytes, stream)
+    if st != PKV_OK:
+        raise PkvError(st, "pkv_restore_from_host_noalloc")
+
+
+def pkv_restore_from_host_noalloc_status(plan: Plan, host_payload, host_payload_bytes, host_scales,
+                                         host_scale_bytes, k_cache, v_cache, cache_bytes, stream=0) -> int:
+    return load().pkv_restore_from_host_noalloc(plan.handle, host_payload, host_payload_bytes, host_scales,
+                                                host_scale_bytes, k_cache, v_cache, cache_bytes, stream or None)
+
+
+def restore_from_host_noalloc_tensors(plan: Plan, host_payload, host_scales, k_cache, v_cache, stream=None) -> None:
+    """Marshal pinned host tensors and device caches into pkv_restore_from_host_noalloc."""
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream(k_cache.device)
+    nbytes = lambda t: t.numel() * t.element_size()
+    pkv_restore_from_host_noalloc(plan, host_payload.data_ptr(), nbytes(host_payload), host_scales.data_ptr(),
+                                  nbytes(host_scales), k_cache.data_ptr(), v_cache.data_ptr(),
+                                  cache_nbytes(k_cache, v_cache), stream.cuda_stream)
 
 
 def pkv_free(plan: Plan) -> None:

@@ -93,6 +93,31 @@ static_assert(kHostCopyStreams >= 1 && kHostCopyStreams <= 32, "copy streams are
 #endif
 constexpr uint64_t kHostChunkBytes = PKV_HOST_CHUNK_BYTES;
 
+// The allocation-free streamed restore stages the checkpoint through a
+// static device buffer: payload windows in its first kStagePayloadBytes, one
+// request-layer's scales in the kStageScaleBytes after them.
+constexpr uint64_t kStagePayloadBytes = 64ull << 20;
+constexpr uint64_t kStageScaleBytes = 4ull << 20;
+
+// One step of that restore, all on the caller's stream: copy the step's
+// scales (if any) and payload ranges from host memory into the stage, then
+// restore units [u0, u1) -- one layer of one request -- whose K rows start in
+// payload bytes [win_lo, win_hi).  A window holds the most consecutive reused
+// blocks, in payload order, that span at most kStagePayloadBytes; payload
+// byte o of the window sits at stage offset o - win_lo.
+struct StageStep {
+  int64_t u0, u1;
+  uint64_t win_lo, win_hi;  // absolute payload bytes
+  uint64_t scale0;          // absolute binary16 element of the request-layer's scales
+  uint64_t scale_elems;     // elements staged before this step (0: none; the stage already holds them)
+  int64_t copy0, copy1;     // its payload copies in HostPlan::stage_copies
+};
+struct StageCopy {
+  uint64_t src;  // absolute payload byte offset
+  uint64_t dst;  // byte offset into the stage
+  uint64_t len;
+};
+
 // Everything the plan needs on the device, built on the host.
 struct HostPlan {
   int32_t kind = 0;  // 0 = restore, 1 = checkpoint write
@@ -113,6 +138,12 @@ struct HostPlan {
   std::vector<int64_t> payload_layer, scale_layer;
   int64_t rotated_rows = 0;  // restore plans: restored rows whose keys rotate (shift != 0)
   std::vector<uint64_t> req_payload_bytes;  // per request: bytes of its checkpoint payload, all layers
+  // Restore plans: the schedule of the restore staged through the library's
+  // static buffer (add_stage_steps in plan.cpp), or stage_ok = false when a
+  // request-layer's scales do not fit it.
+  std::vector<StageStep> stage_steps;
+  std::vector<StageCopy> stage_copies;
+  bool stage_ok = false;
 };
 
 // Restore workgroups resident per compute unit, chosen per plan: 8 to 16

@@ -98,6 +98,39 @@ uint64_t tile_bytes(const pkv_model_t& m, int bits) {
   return uint64_t(m.block_tokens) * m.num_kv_heads * m.head_dim * bits / 8;
 }
 
+// Steps of the staged restore for the units [u0, u1) of one request-layer:
+// windows of the most consecutive reused blocks (payload order, offsets
+// relative to layer_base) that span at most kStagePayloadBytes (one block,
+// at most 16 MiB, always fits), each with its copies (blocks closer than
+// kHostGapBytes merged); the request-layer's scales, if any, go with the
+// first window.
+void add_stage_steps(HostPlan& hp, const std::vector<CopyRange>& blocks, int64_t u0, int64_t u1, uint64_t layer_base,
+                     uint64_t scale0, uint64_t scale_elems) {
+  for (size_t i = 0; i < blocks.size();) {
+    const uint64_t lo = blocks[i].off;
+    size_t j = i + 1;
+    while (j < blocks.size() && blocks[j].off + blocks[j].len - lo <= kStagePayloadBytes) ++j;
+    StageStep st;
+    st.u0 = u0;
+    st.u1 = u1;
+    st.win_lo = layer_base + lo;
+    st.win_hi = layer_base + blocks[j - 1].off + blocks[j - 1].len;
+    st.scale0 = scale0;
+    st.scale_elems = i == 0 ? scale_elems : 0;
+    st.copy0 = int64_t(hp.stage_copies.size());
+    for (size_t a = i; a < j;) {
+      size_t b = a + 1;
+      while (b < j && blocks[b].off - (blocks[b - 1].off + blocks[b - 1].len) <= kHostGapBytes) ++b;
+      const uint64_t c0 = blocks[a].off, c1 = blocks[b - 1].off + blocks[b - 1].len;
+      hp.stage_copies.push_back(StageCopy{layer_base + c0, c0 - lo, c1 - c0});
+      a = b;
+    }
+    st.copy1 = int64_t(hp.stage_copies.size());
+    hp.stage_steps.push_back(st);
+    i = j;
+  }
+}
+
 }  // namespace
 
 int32_t page_shift(const pkv_model_t& m) { return ilog2(m.page_size) + (m.kv_layout == PKV_KV_PAIRED ? 1 : 0); }
@@ -232,6 +265,8 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
   try {
     hp.reqs.resize(num_requests);
     hp.req_payload_bytes.assign(size_t(num_requests), 0);
+    hp.stage_steps.clear();
+    hp.stage_copies.clear();
     hp.tables.resize(size_t(num_requests) * size_t(D));
     // Per request: page table, cos/sin table, block offsets inside a layer.
     std::vector<std::vector<uint64_t>> block_off(num_requests);
@@ -283,8 +318,26 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
     hp.layer_units.assign(1, 0);
     hp.payload_layer.assign(1, 0);
     hp.scale_layer.assign(1, 0);
+    // Staged restore: per request, the reused blocks' K + V tile ranges
+    // relative to a layer's payload start, in payload order.
+    std::vector<std::vector<CopyRange>> reused(static_cast<size_t>(num_requests));
+    std::vector<bool> scales_needed(static_cast<size_t>(num_requests), false);
+    hp.stage_ok = true;
+    for (int32_t r = 0; r < num_requests; ++r) {
+      const pkv_request_t& q = requests[r];
+      const int64_t nb = ceil_div(q.suffix_tokens, B);
+      for (int tag = 0; tag < 4; ++tag)
+        for (int64_t b = 0; b < nb; ++b)
+          if (q.tags[b] == tag && !q.repair_mask[b]) {
+            reused[size_t(r)].push_back(
+                CopyRange{block_off[r][b], tile_bytes(m, kKeyBits[tag]) + tile_bytes(m, kValueBits[tag])});
+            if (tag != PKV_TAG_FP16) scales_needed[size_t(r)] = true;
+          }
+      if (scales_needed[size_t(r)] && uint64_t(nb) * H * 4 * 2 > kStageScaleBytes) hp.stage_ok = false;
+    }
     for (int64_t l = 0; l < L; ++l) {
       for (int32_t r = 0; r < num_requests; ++r) {
+        const int64_t u_begin = int64_t(hp.units.size());
         const pkv_request_t& q = requests[r];
         const int64_t nb = ceil_div(q.suffix_tokens, B);
         const ReqInfo& rd = hp.reqs[r];
@@ -334,6 +387,10 @@ pkv_status_t build_host_plan(const pkv_model_t* model, const pkv_request_t* requ
           hp.info.bytes_read += uint64_t(n_valid) * H * D * (kKeyBits[tag] + kValueBits[tag]) / 8;
           if (tag != PKV_TAG_FP16) hp.info.bytes_read += uint64_t(H) * 4 * 2;
         }
+        if (hp.stage_ok && int64_t(hp.units.size()) > u_begin)
+          add_stage_steps(hp, reused[size_t(r)], u_begin, int64_t(hp.units.size()), layer_base,
+                          scales_needed[size_t(r)] ? (q.scale_offset + uint64_t(l) * nb * H * 4) : 0,
+                          scales_needed[size_t(r)] ? uint64_t(nb) * H * 4 : 0);
       }
       hp.layer_units.push_back(int64_t(hp.units.size()));
       hp.payload_layer.push_back(int64_t(hp.payload_ranges.size()));
@@ -588,6 +645,38 @@ pkv_status_t pkv_internal_stream_schedule(const pkv_model_t* model, const pkv_re
         ++k;
       }
   }
+  return PKV_OK;
+}
+
+// Internal test hook (not part of pkv.h): the schedule of the staged
+// (allocation-free) restore.  steps_out receives 8 int64 per step (u0, u1,
+// win_lo, win_hi, scale0, scale_elems, copy0, copy1), copies_out 3 uint64 per
+// copy (src, dst, len); *stage_ok is 0 when the plan cannot be staged.
+// Counts are returned even when the buffers are short.
+pkv_status_t pkv_internal_stage_schedule(const pkv_model_t* model, const pkv_request_t* requests,
+                                         int32_t num_requests, int64_t* steps_out, int64_t step_capacity,
+                                         uint64_t* copies_out, int64_t copy_capacity, int64_t* n_steps,
+                                         int64_t* n_copies, int32_t* stage_ok) {
+  if (!n_steps || !n_copies || !stage_ok) return PKV_ERR_INVALID_ARGUMENT;
+  pkv::HostPlan hp;
+  pkv_status_t st = pkv::build_host_plan(model, requests, num_requests, &hp);
+  if (st != PKV_OK) return st;
+  *n_steps = int64_t(hp.stage_steps.size());
+  *n_copies = int64_t(hp.stage_copies.size());
+  *stage_ok = hp.stage_ok ? 1 : 0;
+  if (steps_out && step_capacity >= *n_steps)
+    for (size_t i = 0; i < hp.stage_steps.size(); ++i) {
+      const pkv::StageStep& s = hp.stage_steps[i];
+      const int64_t v[8] = {s.u0, s.u1, int64_t(s.win_lo), int64_t(s.win_hi), int64_t(s.scale0),
+                            int64_t(s.scale_elems), s.copy0, s.copy1};
+      memcpy(steps_out + 8 * i, v, sizeof(v));
+    }
+  if (copies_out && copy_capacity >= *n_copies)
+    for (size_t i = 0; i < hp.stage_copies.size(); ++i) {
+      copies_out[3 * i] = hp.stage_copies[i].src;
+      copies_out[3 * i + 1] = hp.stage_copies[i].dst;
+      copies_out[3 * i + 2] = hp.stage_copies[i].len;
+    }
   return PKV_OK;
 }
 

@@ -41,6 +41,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 
 #include "pkv.h"
@@ -65,6 +66,10 @@ struct KernelArgs {
   int32_t H, D, log2P, cols, tpp;
   int32_t R;            // rotary channels per head
   int32_t page_shift;   // slot rows from a layer's start to page p: p << page_shift
+  // Units whose K rows start outside [win_lo, win_hi) payload bytes are
+  // skipped (the staged restore runs a request's layer in payload windows);
+  // [0, 2^64) everywhere else.
+  uint64_t win_lo, win_hi;
 };
 
 __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
@@ -374,6 +379,7 @@ template <bool BF16, int STYLE>
 __global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(KernelArgs a) {
   __shared__ __attribute__((aligned(16))) double s_tab[kMaxHeadDim];
   const Unit u = a.units[xcd_grouped(blockIdx.x, gridDim.x)];
+  if (u.k_off < a.win_lo || u.k_off >= a.win_hi) return;  // uniform across the workgroup
   const int tid = threadIdx.x;
   const int tag = u.tag & 0xFF;
   const bool rot = (u.tag & kUnitRotate) != 0;
@@ -527,11 +533,15 @@ pkv_status_t check_restore_buffers(const pkv_plan* plan, const void* payload, ui
   return PKV_OK;
 }
 
-// Enqueue the restore kernel over units [u0, u0 + n) of the plan.
+// Enqueue the restore kernel over units [u0, u0 + n) of the plan, those whose
+// K rows start in payload bytes [win_lo, win_hi).
 pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const void* scales, void* k_cache,
-                            void* v_cache, int64_t u0, int64_t n, hipStream_t stream) {
+                            void* v_cache, int64_t u0, int64_t n, hipStream_t stream, uint64_t win_lo = 0,
+                            uint64_t win_hi = ~uint64_t(0)) {
   const pkv_model_t& m = plan->host.model;
   KernelArgs a;
+  a.win_lo = win_lo;
+  a.win_hi = win_hi;
   a.units = plan->d_units + u0;
   a.tables = plan->d_tables;
   a.payload = static_cast<const uint8_t*>(payload);
@@ -559,6 +569,50 @@ pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const voi
   return hipGetLastError() == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
 }
 
+}  // namespace pkv
+
+// Staging buffer of pkv_restore_from_host_noalloc: payload windows in the
+// first kStagePayloadBytes, one request-layer's scales after them.  Each GPU
+// the library runs on holds its own copy until the process ends.  In host
+// code this name is not a device address: the entry point takes the address
+// from hipGetSymbolAddress, once per device (stage_address).
+static __device__ __align__(256) unsigned char scratch[pkv::kStagePayloadBytes + pkv::kStageScaleBytes];
+
+namespace pkv {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_stage_mu;
+void* g_stage[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev` (the current device).
+pkv_status_t stage_address(int dev, uint8_t** out) {
+  if (dev < 0 || dev >= kMaxDevices) return PKV_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_stage_mu);
+  if (!g_stage[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return PKV_ERR_DEVICE;
+    }
+    g_stage[dev] = p;
+  }
+  *out = static_cast<uint8_t*>(g_stage[dev]);
+  return PKV_OK;
+}
+
+// Pinned host memory only: asynchronous copies from it need no staging by
+// the runtime.
+bool pinned_host(const void* p) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeHost;
+}
+
+}  // namespace
 }  // namespace pkv
 
 extern "C" {
@@ -677,6 +731,59 @@ pkv_status_t pkv_restore_from_host(const pkv_plan_t* plan, const void* host_payl
     const int64_t u0 = h.layer_units[l], n = h.layer_units[l + 1] - u0;
     if (n == 0) continue;
     st = pkv::launch_restore(plan, payload, scales, k_cache, v_cache, u0, n, stream);
+    if (st != PKV_OK) return st;
+  }
+  return PKV_OK;
+}
+
+pkv_status_t pkv_restore_from_host_noalloc(const pkv_plan_t* plan, const void* host_payload,
+                                           uint64_t host_payload_bytes, const void* host_scales,
+                                           uint64_t host_scale_bytes, void* k_cache, void* v_cache,
+                                           uint64_t cache_bytes, void* hip_stream) {
+  if (!plan || plan->host.kind != 0) return PKV_ERR_INVALID_ARGUMENT;
+  const pkv::HostPlan& h = plan->host;
+  const pkv_plan_info_t& info = h.info;
+  if (info.num_units == 0) return PKV_OK;
+  if (!host_payload || !host_scales || !k_cache || !v_cache) return PKV_ERR_INVALID_ARGUMENT;
+  if (host_payload_bytes < info.payload_bytes || host_scale_bytes < info.scale_bytes || cache_bytes < info.cache_bytes)
+    return PKV_ERR_INVALID_ARGUMENT;
+  pkv::ByteRange caches[2];
+  int n_caches = 0;
+  if (!pkv::cache_ranges(h.model, k_cache, v_cache, info.cache_bytes, caches, n_caches)) return PKV_ERR_INVALID_ARGUMENT;
+  // Size limit: one request-layer's scales must fit the scale stage.
+  if (!h.stage_ok) return PKV_ERR_INVALID_ARGUMENT;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return PKV_ERR_DEVICE;
+  if (!pkv::pinned_host(host_payload) || !pkv::pinned_host(host_scales)) return PKV_ERR_INVALID_ARGUMENT;
+  pkv_status_t st;
+  if ((st = pkv::device_resident(plan, k_cache)) != PKV_OK || (st = pkv::device_resident(plan, v_cache)) != PKV_OK)
+    return st;
+  uint8_t* stage = nullptr;
+  if ((st = pkv::stage_address(dev, &stage)) != PKV_OK) return st;
+  uint8_t* stage_scales = stage + pkv::kStagePayloadBytes;
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  const uint8_t* hp = static_cast<const uint8_t*>(host_payload);
+  const uint8_t* hs = static_cast<const uint8_t*>(host_scales);
+  // Every step goes on the caller's stream, so a step's copies wait for the
+  // restore of the step before it, which still reads the stage.
+  for (const pkv::StageStep& step : h.stage_steps) {
+    if (step.scale_elems &&
+        hipMemcpyAsync(stage_scales, hs + step.scale0 * 2, step.scale_elems * 2, hipMemcpyHostToDevice, stream) !=
+            hipSuccess)
+      return PKV_ERR_DEVICE;
+    for (int64_t c = step.copy0; c < step.copy1; ++c) {
+      const pkv::StageCopy& cp = h.stage_copies[size_t(c)];
+      if (hipMemcpyAsync(stage + cp.dst, hp + cp.src, cp.len, hipMemcpyHostToDevice, stream) != hipSuccess)
+        return PKV_ERR_DEVICE;
+    }
+    // The kernel adds a unit's absolute checkpoint offsets to these bases:
+    // payload byte o of the window is stage byte o - win_lo, scale element e
+    // of the request-layer is stage element e - scale0.
+    const void* payload_base = reinterpret_cast<const void*>(reinterpret_cast<uintptr_t>(stage) - step.win_lo);
+    const void* scales_base =
+        reinterpret_cast<const void*>(reinterpret_cast<uintptr_t>(stage_scales) - step.scale0 * 2);
+    st = pkv::launch_restore(plan, payload_base, scales_base, k_cache, v_cache, step.u0, step.u1 - step.u0, stream,
+                             step.win_lo, step.win_hi);
     if (st != PKV_OK) return st;
   }
   return PKV_OK;

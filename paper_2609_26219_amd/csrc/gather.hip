@@ -475,9 +475,18 @@ __device__ __forceinline__ Quant tile_range(const GatherArgs& a, const TileHdr& 
   return q;
 }
 
-template <bool BF16, int NL>
+// STAGE: the workgroup's waves encode every head of one (block, K|V), whose
+// code tile [B][H][D] is one contiguous run of the checkpoint.  Each wave
+// puts its head's codes into the tile's image in LDS; after a barrier the
+// workgroup writes the image out in whole 16-byte lanes, so every 128-byte
+// line of the tile is written once, by one store instruction (without it, a
+// 4-bit row of one head is half a line, written by a different wave than the
+// other half).  FP16 tiles are stored directly either way (each head row is
+// whole lines).
+template <bool BF16, int NL, bool STAGE>
 __device__ __forceinline__ void tile_store(const GatherArgs& a, const TileHdr& h, int r, int c, bool on,
-                                           const uint4 (&w)[NL], const Quant& q, uint16_t sb, uint16_t zb) {
+                                           const uint4 (&w)[NL], const Quant& q, uint16_t sb, uint16_t zb,
+                                           uint8_t* __restrict__ lds) {
   const uint32_t H = uint32_t(a.H), D = uint32_t(a.D);
   const bool lane0 = (threadIdx.x & 63) == 0;
   const __amdgpu_buffer_rsrc_t out = __builtin_amdgcn_make_buffer_rsrc(h.tile, 0, h.tile_bytes, 0x00020000);
@@ -502,16 +511,32 @@ __device__ __forceinline__ void tile_store(const GatherArgs& a, const TileHdr& h
       uint2 v = make_uint2(encode_word<BF16, 4>(make_uint4(x.x, x.y, 0, 0), q),
                            encode_word<BF16, 4>(make_uint4(x.z, x.w, 0, 0), q));
       v = valid ? v : make_uint2(0, 0);
-      const uint32_t off = store ? (uint32_t(t) * H + uint32_t(h.head)) * D + 8u * uint32_t(c) : kDropOffset;
-      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), out, off, 0, kNonTemporal);
+      const uint32_t at = (uint32_t(t) * H + uint32_t(h.head)) * D + 8u * uint32_t(c);
+      if constexpr (STAGE) {
+        if (store) *reinterpret_cast<uint2*>(lds + at) = v;
+      } else {
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), out, store ? at : kDropOffset, 0,
+                                              kNonTemporal);
+      }
     } else {
       uint32_t v = encode_word<BF16, 8>(x, q);
       v = valid ? v : 0u;
-      const uint32_t off = store ? (uint32_t(t) * H + uint32_t(h.head)) * (D / 2) + 4u * uint32_t(c) : kDropOffset;
-      __builtin_amdgcn_raw_buffer_store_b32(v, out, off, 0, kNonTemporal);
+      const uint32_t at = (uint32_t(t) * H + uint32_t(h.head)) * (D / 2) + 4u * uint32_t(c);
+      if constexpr (STAGE) {
+        if (store) *reinterpret_cast<uint32_t*>(lds + at) = v;
+      } else {
+        __builtin_amdgcn_raw_buffer_store_b32(v, out, store ? at : kDropOffset, 0, kNonTemporal);
+      }
     }
   }
   if (lane0) *h.scale_word = uint32_t(sb) | (uint32_t(zb) << 16);
+  if constexpr (STAGE) {
+    __syncthreads();  // every head's codes are in the image
+    const uint32_t n16 = h.tile_bytes / 16;
+    for (uint32_t i = threadIdx.x; i < n16; i += blockDim.x)
+      __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4*>(lds + 16 * i), out, 16 * i, 0,
+                                             kNonTemporal);
+  }
 }
 
 // 16-load tiles (64-token blocks at head_dim 128) hold 64 registers of rows
@@ -521,9 +546,10 @@ __device__ __forceinline__ void tile_store(const GatherArgs& a, const TileHdr& h
 // spilled) and 37% faster than the general kernel on the 70B-shaped write.
 constexpr int kTile16Threads = 512;
 
-template <bool BF16, int NL>
+template <bool BF16, int NL, bool STAGE>
 __global__ __launch_bounds__(NL == 16 ? kTile16Threads : kGatherMaxWaves * 64) void gather_tile_kernel(TileArgs s,
                                                                              const Unit* __restrict__ units) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t tile_image[];
   const GatherArgs& a = s.g;
   const int lane = threadIdx.x & 63;
   const int r = lane / a.lpr;
@@ -537,24 +563,31 @@ __global__ __launch_bounds__(NL == 16 ? kTile16Threads : kGatherMaxWaves * 64) v
   uint16_t sb, zb;
   load_tile<NL>(a, h, r, c, w);
   const Quant q = tile_range<BF16, NL>(a, h, r, w, sb, zb);
-  tile_store<BF16, NL>(a, h, r, c, on, w, q, sb, zb);
+  tile_store<BF16, NL, STAGE>(a, h, r, c, on, w, q, sb, zb, tile_image);
 }
 
+// The staged store needs a workgroup to hold exactly the heads of one
+// (block, K|V) -- one wave per head -- and the 8-bit image of a tile in LDS.
+constexpr uint32_t kTileImageMax = 64u << 10;
+
 template <bool BF16, int NL>
-hipError_t launch_tile_nl(const TileArgs& s, const Unit* units, int wg, hipStream_t stream) {
+hipError_t launch_tile_nl(const TileArgs& s, const Unit* units, int wg, uint32_t image, hipStream_t stream) {
   const int64_t waves = wg / 64;
   const dim3 grid(static_cast<uint32_t>((s.num_tiles + waves - 1) / waves));
-  hipLaunchKernelGGL((gather_tile_kernel<BF16, NL>), grid, dim3(wg), 0, stream, s, units);
+  if (image)
+    hipLaunchKernelGGL((gather_tile_kernel<BF16, NL, true>), grid, dim3(wg), image, stream, s, units);
+  else
+    hipLaunchKernelGGL((gather_tile_kernel<BF16, NL, false>), grid, dim3(wg), 0, stream, s, units);
   return hipGetLastError();
 }
 
 template <bool BF16>
-hipError_t launch_tile(const TileArgs& s, const Unit* units, int nl, int wg, hipStream_t stream) {
+hipError_t launch_tile(const TileArgs& s, const Unit* units, int nl, int wg, uint32_t image, hipStream_t stream) {
   switch (nl) {
-    case 2: return launch_tile_nl<BF16, 2>(s, units, wg, stream);
-    case 4: return launch_tile_nl<BF16, 4>(s, units, wg, stream);
-    case 8: return launch_tile_nl<BF16, 8>(s, units, wg, stream);
-    default: return launch_tile_nl<BF16, 16>(s, units, wg, stream);
+    case 2: return launch_tile_nl<BF16, 2>(s, units, wg, image, stream);
+    case 4: return launch_tile_nl<BF16, 4>(s, units, wg, image, stream);
+    case 8: return launch_tile_nl<BF16, 8>(s, units, wg, image, stream);
+    default: return launch_tile_nl<BF16, 16>(s, units, wg, image, stream);
   }
 }
 
@@ -648,9 +681,12 @@ pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, co
     pkv::TileArgs sa;
     sa.g = a;
     sa.num_tiles = info.num_units * 2 * m.num_kv_heads;
+    // Staged stores when a workgroup is one wave per head of one (block, K|V).
+    const uint64_t image = uint64_t(m.block_tokens) * m.num_kv_heads * m.head_dim;
+    const uint32_t stage = plan->host.workgroup == 64 * m.num_kv_heads && image <= pkv::kTileImageMax ? uint32_t(image) : 0;
     const hipError_t e = m.out_dtype == PKV_OUT_BF16
-                             ? pkv::launch_tile<true>(sa, plan->d_units, nl, plan->host.workgroup, stream)
-                             : pkv::launch_tile<false>(sa, plan->d_units, nl, plan->host.workgroup, stream);
+                             ? pkv::launch_tile<true>(sa, plan->d_units, nl, plan->host.workgroup, stage, stream)
+                             : pkv::launch_tile<false>(sa, plan->d_units, nl, plan->host.workgroup, stage, stream);
     return e == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
   }
   const dim3 grid(static_cast<uint32_t>(2 * info.num_units)), block(plan->host.workgroup);

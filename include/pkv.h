@@ -108,7 +108,8 @@ typedef enum { PKV_KV_SEPARATE = 0, PKV_KV_PAIRED = 1 } pkv_kv_layout_t;
  *   num_layers >= 1; 1 <= num_kv_heads; head_dim % 16 == 0, 16 <= head_dim <= 512;
  *   num_kv_heads * head_dim <= 4096; 1 <= block_tokens <= 1024;
  *   (block_tokens * num_kv_heads * head_dim) % 32 == 0 (every tile 16-byte aligned);
- *   page_size a power of two in [1, 2^20]; pool_pages >= 1;
+ *   page_size a power of two in [1, 2^20], one page of one cache at most 2 GiB
+ *   (page_size * num_kv_heads * head_dim * 2 <= 2^31 bytes); pool_pages >= 1;
  *   rope_theta finite and > 0; out_dtype a pkv_out_dtype_t value;
  *   rope_style a pkv_rope_style_t value; rotary_dim 0 (= head_dim) or a
  *   multiple of 16 in [16, head_dim]; inv_freq NULL or rotary_dim/2 finite

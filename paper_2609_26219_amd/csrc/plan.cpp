@@ -36,6 +36,8 @@ pkv_status_t check_model(const pkv_model_t* m) {
   if (m->block_tokens < 1 || m->block_tokens > kMaxBlockTokens) return PKV_ERR_INVALID_ARGUMENT;
   if ((int64_t(m->block_tokens) * m->num_kv_heads * m->head_dim) % 32 != 0) return PKV_ERR_INVALID_ARGUMENT;
   if (!is_pow2(m->page_size) || m->page_size > (1 << 20)) return PKV_ERR_INVALID_ARGUMENT;
+  // One page of one cache is at most 2 GiB: the kernels address inside a page with 32-bit offsets.
+  if (int64_t(m->page_size) * m->num_kv_heads * m->head_dim * 2 > (int64_t(1) << 31)) return PKV_ERR_INVALID_ARGUMENT;
   if (m->pool_pages < 1) return PKV_ERR_INVALID_ARGUMENT;
   if (!(isfinite(m->rope_theta) && m->rope_theta > 0.0)) return PKV_ERR_INVALID_ARGUMENT;
   if (m->out_dtype != PKV_OUT_FP16 && m->out_dtype != PKV_OUT_BF16) return PKV_ERR_INVALID_ARGUMENT;

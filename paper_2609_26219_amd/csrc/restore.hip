@@ -85,24 +85,38 @@ __device__ __forceinline__ float to_float(double d) {
   return f;
 }
 
+// Loads and stores are buffer instructions: a unit's payload runs and its
+// destination page are uniform bases (scalar registers), each thread keeps
+// one 32-bit offset per run, and a thread's later tokens add a uniform
+// scalar offset -- no per-access 64-bit address arithmetic.  A page of one
+// cache is at most 2 GiB (checked at plan time), so offsets fit 32 bits.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0xFFFFFFFF, 0x00020000);
+}
+// Cache-policy operand of the buffer intrinsics: nt (non-temporal) on gfx950.
+constexpr int kNonTemporal = 2;
+
 // Restored rows are written once and not read again by this launch: store
 // them non-temporally (measured 2% faster on the 8B-shaped workload).
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ void store_row_piece(uint16_t* p, uint4 v) {
-  const u32x4 w = {v.x, v.y, v.z, v.w};
-  __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(p));
+__device__ __forceinline__ void store_row_piece(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, kNonTemporal);
 }
 
+// Two floats to two bfloat16 / binary16 values, round to nearest even, in
+// one packed conversion (v_cvt_pk_bf16_f32 / v_cvt_pk_f16_f32 on gfx950;
+// converting each value alone takes a conversion each plus a shift and an or).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 template <bool BF16>
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
+  const f32x2 v = {a, b};
   if constexpr (BF16) {
-    const uint16_t x = __builtin_bit_cast(uint16_t, static_cast<__bf16>(a));
-    const uint16_t y = __builtin_bit_cast(uint16_t, static_cast<__bf16>(b));
-    return uint32_t(x) | (uint32_t(y) << 16);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
   } else {
-    const uint16_t x = __builtin_bit_cast(uint16_t, static_cast<_Float16>(a));
-    const uint16_t y = __builtin_bit_cast(uint16_t, static_cast<_Float16>(b));
-    return uint32_t(x) | (uint32_t(y) << 16);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2));
   }
 }
 
@@ -121,9 +135,8 @@ struct Chunk8<16> {
   uint4 w;
   // FP16 runs load non-temporally: 1.4% faster on an all-FP16 checkpoint
   // (code runs measured 2-3% slower that way, so they keep the default).
-  __device__ __forceinline__ void load(const uint8_t* p) {
-    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-    w = make_uint4(v.x, v.y, v.z, v.w);
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    w = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kNonTemporal));
   }
   __device__ __forceinline__ uint32_t raw(int e) const {
     const uint32_t word = e < 2 ? w.x : e < 4 ? w.y : e < 6 ? w.z : w.w;
@@ -133,14 +146,24 @@ struct Chunk8<16> {
 template <>
 struct Chunk8<8> {
   uint2 w;
-  __device__ __forceinline__ void load(const uint8_t* p) { w = *reinterpret_cast<const uint2*>(p); }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    w = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+  }
   __device__ __forceinline__ uint32_t raw(int e) const { return ((e < 4 ? w.x : w.y) >> (8 * (e & 3))) & 0xFFu; }
 };
 template <>
 struct Chunk8<4> {
   uint32_t w;
-  __device__ __forceinline__ void load(const uint8_t* p) { w = *reinterpret_cast<const uint32_t*>(p); }
-  __device__ __forceinline__ uint32_t raw(int e) const { return (w >> (4 * e)) & 0xFu; }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    w = __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+  }
+  // Element 2k is the low nibble of byte k, element 2k + 1 its high nibble:
+  // mask the word into four byte-wide codes of each parity, so each code
+  // converts with one v_cvt_f32_ubyte (no bit-field extract per code).
+  __device__ __forceinline__ uint32_t raw(int e) const {
+    const uint32_t bytes = (e & 1 ? w >> 4 : w) & 0x0F0F0F0Fu;
+    return (bytes >> (8 * (e >> 1))) & 0xFFu;
+  }
 };
 
 // Decode element e of a chunk to float (exact for codes <= 255 and binary16).
@@ -221,7 +244,8 @@ __device__ __forceinline__ void decode_run(const Chunk8<KBITS>& c, float s, floa
 // rotate, round, store.
 template <int KBITS, bool ROT, int STYLE, bool BF16>
 __device__ __forceinline__ void key_store(const Chunk8<KBITS>& lo, const Chunk8<KBITS>& hi, const KeyPiece& p, float ks,
-                                          float kz, const double2* __restrict__ cs, uint16_t* __restrict__ dst) {
+                                          float kz, const double2* __restrict__ cs, __amdgpu_buffer_rsrc_t dst,
+                                          uint32_t doff, uint32_t soff) {
   uint4 out_lo, out_hi;
   if constexpr (KBITS == 16 && !ROT && !BF16) {
     // binary16 in, binary16 out, no rotation: the bits are the result.
@@ -259,14 +283,14 @@ __device__ __forceinline__ void key_store(const Chunk8<KBITS>& lo, const Chunk8<
     out_lo = pack8<BF16>(a);
     out_hi = pack8<BF16>(b);
   }
-  store_row_piece(dst + p.lo, out_lo);
-  store_row_piece(dst + p.hi, out_hi);
+  store_row_piece(dst, doff + 2 * p.lo, soff, out_lo);
+  store_row_piece(dst, doff + 2 * p.hi, soff, out_hi);
 }
 
 // Values of one (token, head), piece j (never rotated).
 template <int VBITS, bool BF16>
 __device__ __forceinline__ void value_store(const Chunk8<VBITS>& lo, const Chunk8<VBITS>& hi, int j, int D, float vs,
-                                            float vz, uint16_t* __restrict__ dst) {
+                                            float vz, __amdgpu_buffer_rsrc_t dst, uint32_t doff, uint32_t soff) {
   uint4 out_lo, out_hi;
   if constexpr (VBITS == 16 && !BF16) {
     out_lo = lo.w;
@@ -281,8 +305,8 @@ __device__ __forceinline__ void value_store(const Chunk8<VBITS>& lo, const Chunk
     out_lo = pack8<BF16>(a);
     out_hi = pack8<BF16>(b);
   }
-  store_row_piece(dst + 8 * j, out_lo);
-  store_row_piece(dst + D / 2 + 8 * j, out_hi);
+  store_row_piece(dst, doff + 16 * j, soff, out_lo);
+  store_row_piece(dst, doff + D + 16 * j, soff, out_hi);
 }
 
 // What a thread needs for every token of its unit.
@@ -290,40 +314,41 @@ struct Piece {
   int head, j;
   KeyPiece kp;
   float ks, kz, vs, vz;
-  int64_t pbase;  // cache element offset of the unit's page, in its layer, at the thread's head
+  __amdgpu_buffer_rsrc_t kdst, vdst;  // the unit's destination page in each cache
+  uint32_t doff;                      // bytes from the page's start to the thread's first token, its head
 };
 
 // NK tokens of one thread (t, t + tpp, ...): every load is issued before the
 // first store, so a wave keeps NK tokens of payload in flight.  No load
-// depends on another: the unit's page comes with its work item.
+// depends on another: the unit's page comes with its work item.  Token k of
+// the thread is k * tpp rows further in the payload and in the page.
 template <int NK, int TAG, bool ROT, int STYLE, bool BF16>
 __device__ __forceinline__ void restore_tokens(const KernelArgs& a, const Unit& u, int t, const Piece& q,
                                                const double2* __restrict__ cs) {
   constexpr int KB = kKeyBits[TAG];
   constexpr int VB = kValueBits[TAG];
-  const int H = a.H, D = a.D;
-  const uint8_t* kbase = a.payload + u.k_off;
-  const uint8_t* vbase = a.payload + u.v_off;
-  const int64_t slot_mask = (int64_t(1) << a.log2P) - 1;
-  const int64_t row_elems = int64_t(H) * D;
+  const uint32_t H = uint32_t(a.H), D = uint32_t(a.D), tpp = uint32_t(a.tpp);
+  const __amdgpu_buffer_rsrc_t kr = raw_rsrc(a.payload + u.k_off);
+  const __amdgpu_buffer_rsrc_t vr = raw_rsrc(a.payload + u.v_off);
+  const uint32_t row = uint32_t(t) * H + uint32_t(q.head);  // the thread's first (token, head) row of the unit
+  const uint32_t k_lo = row * (D * KB / 8) + uint32_t(q.kp.lo) * KB / 8;
+  const uint32_t k_hi = row * (D * KB / 8) + uint32_t(q.kp.hi) * KB / 8;
+  const uint32_t v_lo = row * (D * VB / 8) + uint32_t(8 * q.j) * VB / 8;
+  const uint32_t v_hi = v_lo + (D / 2) * VB / 8;
+  const uint32_t doff = q.doff + uint32_t(t) * H * D * 2;
   Chunk8<KB> klo[NK], khi[NK];
   Chunk8<VB> vlo[NK], vhi[NK];
-  int64_t dst[NK];
 #pragma unroll
   for (int k = 0; k < NK; ++k) {
-    const int tk = t + k * a.tpp;
-    const int64_t row = u.row0 + tk;
-    dst[k] = q.pbase + (row & slot_mask) * row_elems;
-    const int64_t r = int64_t(tk) * H + q.head;
-    klo[k].load(kbase + r * (D * KB / 8) + q.kp.lo * KB / 8);
-    khi[k].load(kbase + r * (D * KB / 8) + q.kp.hi * KB / 8);
-    vlo[k].load(vbase + r * (D * VB / 8) + (8 * q.j) * VB / 8);
-    vhi[k].load(vbase + r * (D * VB / 8) + (D / 2 + 8 * q.j) * VB / 8);
+    klo[k].load(kr, k_lo, k * tpp * H * D * KB / 8);
+    khi[k].load(kr, k_hi, k * tpp * H * D * KB / 8);
+    vlo[k].load(vr, v_lo, k * tpp * H * D * VB / 8);
+    vhi[k].load(vr, v_hi, k * tpp * H * D * VB / 8);
   }
 #pragma unroll
   for (int k = 0; k < NK; ++k) {
-    key_store<KB, ROT, STYLE, BF16>(klo[k], khi[k], q.kp, q.ks, q.kz, cs, a.k_cache + dst[k]);
-    value_store<VB, BF16>(vlo[k], vhi[k], q.j, D, q.vs, q.vz, a.v_cache + dst[k]);
+    key_store<KB, ROT, STYLE, BF16>(klo[k], khi[k], q.kp, q.ks, q.kz, cs, q.kdst, doff, k * tpp * H * D * 2);
+    value_store<VB, BF16>(vlo[k], vhi[k], q.j, D, q.vs, q.vz, q.vdst, doff, k * tpp * H * D * 2);
   }
 }
 
@@ -343,8 +368,10 @@ __device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u,
     q.vz = half_bits_to_float(sw.y >> 16);
   }
   // A unit's rows share one page, carried in its work item.
-  q.pbase = int64_t(u.layer) * a.layer_elems + (int64_t(u.page1) << a.page_shift) * (int64_t(a.H) * a.D) +
-            int64_t(head) * a.D;
+  const int64_t page = int64_t(u.layer) * a.layer_elems + (int64_t(u.page1) << a.page_shift) * (int64_t(a.H) * a.D);
+  q.kdst = raw_rsrc(a.k_cache + page);
+  q.vdst = raw_rsrc(a.v_cache + page);
+  q.doff = (uint32_t(u.row0 & ((int64_t(1) << a.log2P) - 1)) * uint32_t(a.H) + uint32_t(head)) * uint32_t(a.D) * 2;
   double2 cs[8];  // (cos, sin) of this thread's eight rotary pairs
   if constexpr (ROT) {
 #pragma unroll

@@ -113,6 +113,16 @@ def test_bad_model(field, value):
     assert _status(shape, reqs) == pb.PKV_ERR_INVALID_ARGUMENT
 
 
+def test_page_of_one_cache_at_most_2gib():
+    """The kernels address inside a page with 32-bit offsets: a page of
+    P * H * D * 2 bytes above 2 GiB is refused, exactly 2 GiB is accepted."""
+    import dataclasses
+    shape, reqs = _base()
+    big = dataclasses.replace(shape, page_size=1 << 20, num_kv_heads=8, head_dim=128, pool_pages=1)
+    assert _status(big, []) == VALID  # 2^20 * 1024 * 2 = 2 GiB
+    assert _status(dataclasses.replace(big, num_kv_heads=16), []) == pb.PKV_ERR_INVALID_ARGUMENT
+
+
 def test_tile_alignment_rule():
     import dataclasses
     shape, reqs = _base()

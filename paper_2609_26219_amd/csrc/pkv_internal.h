@@ -148,24 +148,24 @@ struct HostPlan {
 
 // Restore workgroups resident per compute unit, chosen per plan: 8 to 16
 // waves (for 4-wave workgroups two to four, one wave per SIMD each; 16 waves
-// is the register limit).  Measured on the 8B-shaped
-// 32-layer restore, paired pages, destination rows 7 slots into a page
-// (units of 9, 16 and 7 tokens), us for 2/3/4:
-//   FP16 (read:write 1.00)  1227-1235 / 1277 / 1282-1290
-//   K8V8 (0.50)              922-942 /  891 /  929-942
-//   mixed (0.47)             936-978 /  908 /  952
-//   K8V4 (0.38)              892-931 /  870 /  886-889
-//   K4V4 (0.25)              931-963 /  830 /  808
-// and with page-aligned rows (16-token units) 902-921 / 960-966 / 958 for
-// the mixed tags, 765-771 / 827-838 / 838-846 for K4V4: the best count falls
-// as units grow.  With no shift (no rotation, no table) the same unaligned
-// plans run best with fewer: mixed 900 / 961 / 978, K8V8 876 / 958 / 967,
-// K8V4 835-839 / 914-918 / 925, K4V4 820 / 802 / 836-842; and so do the
-// shifted ones into separate K and V caches: mixed 968-973 / 1004-1013 /
-// 1032, K8V8 949 / 1019-1022 / 1026-1033, K8V4 910-916 / 945-948 / 972,
-// K4V4 935-939 / 847-848 / 876-878.  The one-head-per-GPU share of the same
-// workload restores in 139 us (16 one-wave workgroups) whatever the target,
-// the two-head share in 263 us at 8 one-wave workgroups and 243 at 12 or 16.
+// is the register limit).  Measured on the 8B-shaped 32-layer restore,
+// destination rows 7 slots into a page (units of 9, 16 and 7 tokens), us at
+// 2 / 3 / 4 workgroups per CU, paired pages:
+//   FP16 (read:write 1.00)  1200-1208 / 1233-1248 / 1240-1250
+//   K8V8 (0.50)              889-892 /  915-916 /  956-958
+//   mixed (0.47)             906-953 /  905-913 /  941-952
+//   K8V4 (0.38)              861-867 /  836-837 /  884-885
+//   K4V4 (0.25)              874-875 /      780 /  806-816
+// separate caches:
+//   FP16 1311-1325 / 1333-1347 / 1333-1349, K8V8 963 / 1041 / 1050-1053,
+//   mixed 973-991 / 1015-1030 / 1039-1046, K8V4 907-908 / 954-957 / 979-980,
+//   K4V4 895-896 / 851-856 / 896-899;
+// and with page-aligned rows (16-token units), paired: mixed 891-898 /
+// 952-961 / 965, K4V4 774-776 / 836-837 / 847: the best count falls as units
+// grow.  Unshifted plans (no rotation, no table) run best with fewer.  The
+// one-head-per-GPU share of the same workload restores in 139 us (16 one-wave
+// workgroups) whatever the target, the two-head share in 263 us at 8
+// one-wave workgroups and 243 at 12 or 16.
 int restore_workgroups_per_cu(const HostPlan& hp);
 
 // Validate and build the host side of a plan.  Makes no HIP call.

@@ -162,8 +162,9 @@ bool cache_ranges(const pkv_model_t& m, const void* k_cache, const void* v_cache
 
 int restore_workgroups_per_cu(const HostPlan& hp) {
   // The memory system streams best with about 32K output elements of work in
-  // flight per compute unit (two thirds of that for read-heavy plans, six
-  // fifths for write-heavy ones; three quarters for units that do not rotate
+  // flight per compute unit (two thirds of that for plans reading half a byte
+  // or more per byte written, 1.14x for those reading under 0.3; three
+  // quarters for units that do not rotate
   // their keys, and again for separate K and V caches; half again for rows
   // narrow enough to take workgroups under 256 threads): so many units at a
   // time, between 8 and 16 waves' worth (two to four 4-wave workgroups).
@@ -174,7 +175,7 @@ int restore_workgroups_per_cu(const HostPlan& hp) {
   const double ratio = double(info.bytes_read) / double(info.bytes_written);
   const double rotated = double(hp.rotated_rows) / double(info.restored_rows);
   const double target =
-      32768.0 * (ratio >= 0.75 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 1.2) * (0.75 + 0.25 * rotated) *
+      32768.0 * (ratio >= 0.49 ? 2.0 / 3.0 : ratio >= 0.3 ? 1.0 : 1.14) * (0.75 + 0.25 * rotated) *
       (hp.model.kv_layout == PKV_KV_SEPARATE ? 0.75 : 1.0) * (hp.workgroup < kWorkgroup ? 1.5 : 1.0);
   const double unit_elems =
       double(info.restored_rows) * hp.model.num_kv_heads * hp.model.head_dim / double(info.num_units);

@@ -64,6 +64,7 @@ struct KernelArgs {
   uint16_t* v_cache;
   int64_t layer_elems;  // elements of one layer of a cache: pool_pages * P * H * D, twice that when paired
   int32_t H, D, log2P, cols, tpp;
+  int32_t cols_shift, dq_shift;  // log2 of cols and of D/16 when they are powers of two, else -1
   int32_t R;            // rotary channels per head
   int32_t page_shift;   // slot rows from a layer's start to page p: p << page_shift
   // Units whose K rows start outside [win_lo, win_hi) payload bytes are
@@ -414,11 +415,13 @@ __global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(Ker
     for (int i = tid; i < a.D; i += int(blockDim.x)) s_tab[i] = a.tables[u.table_off + i];
     __syncthreads();
   }
-  const int t0 = tid / a.cols;
+  // Thread -> (token, head, piece): shifts when the row's piece counts are
+  // powers of two (uniform branches), divisions otherwise.
+  const int t0 = a.cols_shift >= 0 ? tid >> a.cols_shift : tid / a.cols;
   if (t0 >= a.tpp) return;
   const int c = tid - t0 * a.cols;
   const int dq = a.D >> 4;
-  const int head = c / dq;
+  const int head = a.dq_shift >= 0 ? c >> a.dq_shift : c / dq;
   const int j = c - head * dq;
   switch (tag * 2 + (rot ? 1 : 0)) {
     case 0: restore_unit<PKV_TAG_FP16, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
@@ -582,6 +585,13 @@ pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const voi
   a.log2P = plan->host.log2_page;
   a.cols = m.num_kv_heads * m.head_dim / 16;
   a.tpp = plan->host.workgroup / a.cols;
+  auto shift_of = [](int32_t x) {
+    int32_t s = 0;
+    while ((1 << s) < x) ++s;
+    return (1 << s) == x ? s : -1;
+  };
+  a.cols_shift = shift_of(a.cols);
+  a.dq_shift = shift_of(m.head_dim / 16);
   a.R = m.rotary_dim ? m.rotary_dim : m.head_dim;
   const dim3 grid(static_cast<uint32_t>(n)), block(plan->host.workgroup);
   const bool bf16 = m.out_dtype == PKV_OUT_BF16, half = m.rope_style == PKV_ROPE_HALF;

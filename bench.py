@@ -407,6 +407,32 @@ def host_restore(torch, binding, dr, steps: int, stream):
     }
 
 
+def checkpoint_to_host(torch, binding, ck, old, stream, steps: int):
+    """The checkpoint write straight into pinned host memory (where the paper
+    keeps checkpoints): the kernel stores the checkpoint over the host link,
+    no staging copy.  Its output is checked against the device-written one."""
+    hp = torch.empty(ck.payload.numel(), dtype=torch.uint8, pin_memory=True)
+    hs = torch.empty(ck.scales.numel(), dtype=torch.int16, pin_memory=True)
+    run = lambda i: binding.quantize_gather_tensors(ck.plan, old.k, old.v, hp, hs, stream)
+    ms, _ = time_launches(torch, run, steps, 2, stream)
+    avg = sum(ms) / len(ms)
+    same = bool(torch.equal(hp.to(ck.payload.device), ck.payload) and torch.equal(hs.to(ck.scales.device), ck.scales))
+    written = int(ck.info["bytes_written"])
+    log(f"[bench] checkpoint write into pinned host memory: {avg:.2f} ms, {written / (avg * 1e-3) / 1e9:.1f} GB/s "
+        f"over the host link, identical to the device-written checkpoint: {same}")
+    return {
+        "what": "the same pkv_quantize_gather launch with payload and scales in pinned host memory: the kernel "
+                "writes the checkpoint over the host link",
+        "ms": round(avg, 3),
+        "ms_p10_p50_p90": [round(ms[int(q * (len(ms) - 1))], 3) for q in (0.1, 0.5, 0.9)],
+        "launches": len(ms),
+        "bytes_written_over_link": written,
+        "GBps": round(written / (avg * 1e-3) / 1e9, 2),
+        "frac_of_pcie_peak": round(written / (avg * 1e-3) / 1e9 / PCIE_PEAK_GBPS, 4),
+        "identical_to_device_write": same,
+    }
+
+
 def planner_timing(binding, case, reps: int = 20):
     """Resume planner (pkv_plan_repair, host C++) on each request of the
     workload: dirty window d_hat = 12% of the suffix, kappa = 1.5%, stored
@@ -679,6 +705,8 @@ def run(args, pool, n_workers):
                                             GATHER_SRC),
             },
         }
+        if args.host_steps > 0:
+            checkpoint_write["to_pinned_host"] = checkpoint_to_host(torch, binding, ck, old, stream, args.host_steps)
         ck.old = None
         sets = [DeviceRestore(case, checkpoint=(ck.payload, ck.scales)) for _ in range(max(1, args.sets))]
         del ck

@@ -101,8 +101,16 @@ constexpr int kNonTemporal = 2;
 
 // Restored rows are written once and not read again by this launch: store
 // them non-temporally (measured 2% faster on the 8B-shaped workload).
+//
+// The whole offset goes in the VGPR operand and the SGPR offset is 0.  A
+// 16-byte store reads its data registers after it issues, so an instruction
+// right behind it must not overwrite them; the compiler inserts the wait
+// state for that only when the store's SGPR offset is a constant, and with
+// a register SGPR offset gfx950 was seen storing the next instruction's
+// result (a token's 16 outputs replaced, now and then, by an address or a
+// decoded value).
 __device__ __forceinline__ void store_row_piece(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, kNonTemporal);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff + soff, 0, kNonTemporal);
 }
 
 // Two floats to two bfloat16 / binary16 values, round to nearest even, in

@@ -41,6 +41,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 #include <new>
 
@@ -93,9 +94,15 @@ __device__ __forceinline__ float to_float(double d) {
 // cache is at most 2 GiB (checked at plan time), so offsets fit 32 bits.
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, 0xFFFFFFFF, 0x00020000);
+// A buffer of `bytes` bytes from `base`: loads past its end return 0 and
+// stores past it are dropped by the hardware, with no memory access.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
 }
+constexpr uint32_t kWholeRange = 0xFFFFFFFFu;
+// An offset past every bounded buffer of the kernel (a cache page is below
+// 2 GiB, a unit's payload run a few MiB): accesses there are dropped.
+constexpr uint32_t kOutside = 0x80000000u;
 // Cache-policy operand of the buffer intrinsics: nt (non-temporal) on gfx950.
 constexpr int kNonTemporal = 2;
 
@@ -327,18 +334,66 @@ struct Piece {
   uint32_t doff;                      // bytes from the page's start to the thread's first token, its head
 };
 
+// Two orders of a workgroup's start.
+//
+// Early (launches larger than the chip holds at once): the request's (cos,
+// sin) table is staged in LDS behind a barrier at the start, then each
+// thread loads its head's scales, then issues its payload loads.  Other
+// resident workgroups hide that chain of dependent loads.
+//
+// Late (launches whose workgroups are all resident at once, where nothing
+// hides it): table entry tid and the head's scale word are loaded at the
+// start, the payload loads are issued right after, and only then are the
+// table entries written to LDS, the barrier passed and the scales
+// converted.  The table, the scales and the payload are then in flight
+// together: one memory latency before the first store instead of three.
+// Every wave passes the barrier exactly once, as the token-count switch is
+// wave-uniform in this order (restore_unit).
+struct Stage {
+  double* s_tab;        // LDS, D doubles
+  const double* table;  // the request's table in global memory
+  double tval;          // entry tid (threads < D)
+  uint2 sw;             // the thread's head: K scale, K zero, V scale, V zero (binary16)
+  bool pending;         // not yet staged (uniform across the workgroup)
+  int tid, D, threads;
+};
+
+template <int TAG, bool ROT>
+__device__ __forceinline__ void finish_stage(Stage& st, Piece& q, double2* cs) {
+  if (!st.pending) return;
+  if constexpr (ROT) {
+    if (st.tid < st.D) st.s_tab[st.tid] = st.tval;
+    for (int i = st.tid + st.threads; i < st.D; i += st.threads) st.s_tab[i] = st.table[i];
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cs[e] = *reinterpret_cast<const double2*>(st.s_tab + 2 * (8 * q.j + e));
+  }
+  if constexpr (TAG != PKV_TAG_FP16) {
+    uint2 sw = st.sw;
+    asm volatile("" : "+v"(sw.x), "+v"(sw.y));  // keeps the conversion behind the payload loads
+    q.ks = half_bits_to_float(sw.x & 0xFFFFu);
+    q.kz = half_bits_to_float(sw.x >> 16);
+    q.vs = half_bits_to_float(sw.y & 0xFFFFu);
+    q.vz = half_bits_to_float(sw.y >> 16);
+  }
+  st.pending = false;
+}
+
 // NK tokens of one thread (t, t + tpp, ...): every load is issued before the
 // first store, so a wave keeps NK tokens of payload in flight.  No load
 // depends on another: the unit's page comes with its work item.  Token k of
-// the thread is k * tpp rows further in the payload and in the page.
-template <int NK, int TAG, bool ROT, int STYLE, bool BF16>
-__device__ __forceinline__ void restore_tokens(const KernelArgs& a, const Unit& u, int t, const Piece& q,
-                                               const double2* __restrict__ cs) {
+// the thread is k * tpp rows further in the payload and in the page.  In the
+// late order only the first `valid` tokens are real: the accesses of the
+// others get offsets past their buffers, which the hardware drops.
+template <int NK, int TAG, bool ROT, int STYLE, bool BF16, bool LATE>
+__device__ __forceinline__ void restore_tokens(const KernelArgs& a, const Unit& u, int t, Piece& q,
+                                               double2* __restrict__ cs, Stage& st, int valid) {
   constexpr int KB = kKeyBits[TAG];
   constexpr int VB = kValueBits[TAG];
   const uint32_t H = uint32_t(a.H), D = uint32_t(a.D), tpp = uint32_t(a.tpp);
-  const __amdgpu_buffer_rsrc_t kr = raw_rsrc(a.payload + u.k_off);
-  const __amdgpu_buffer_rsrc_t vr = raw_rsrc(a.payload + u.v_off);
+  const uint32_t rows = uint32_t(u.n_valid) * H;
+  const __amdgpu_buffer_rsrc_t kr = raw_rsrc(a.payload + u.k_off, LATE ? rows * (D * KB / 8) : kWholeRange);
+  const __amdgpu_buffer_rsrc_t vr = raw_rsrc(a.payload + u.v_off, LATE ? rows * (D * VB / 8) : kWholeRange);
   const uint32_t row = uint32_t(t) * H + uint32_t(q.head);  // the thread's first (token, head) row of the unit
   const uint32_t k_lo = row * (D * KB / 8) + uint32_t(q.kp.lo) * KB / 8;
   const uint32_t k_hi = row * (D * KB / 8) + uint32_t(q.kp.hi) * KB / 8;
@@ -349,27 +404,30 @@ __device__ __forceinline__ void restore_tokens(const KernelArgs& a, const Unit& 
   Chunk8<VB> vlo[NK], vhi[NK];
 #pragma unroll
   for (int k = 0; k < NK; ++k) {
-    klo[k].load(kr, k_lo, k * tpp * H * D * KB / 8);
-    khi[k].load(kr, k_hi, k * tpp * H * D * KB / 8);
-    vlo[k].load(vr, v_lo, k * tpp * H * D * VB / 8);
-    vhi[k].load(vr, v_hi, k * tpp * H * D * VB / 8);
+    const bool on = !LATE || k < valid;
+    klo[k].load(kr, on ? k_lo : kOutside, k * tpp * H * D * KB / 8);
+    khi[k].load(kr, on ? k_hi : kOutside, k * tpp * H * D * KB / 8);
+    vlo[k].load(vr, on ? v_lo : kOutside, k * tpp * H * D * VB / 8);
+    vhi[k].load(vr, on ? v_hi : kOutside, k * tpp * H * D * VB / 8);
   }
+  if constexpr (LATE) finish_stage<TAG, ROT>(st, q, cs);
 #pragma unroll
   for (int k = 0; k < NK; ++k) {
-    key_store<KB, ROT, STYLE, BF16>(klo[k], khi[k], q.kp, q.ks, q.kz, cs, q.kdst, doff, k * tpp * H * D * 2);
-    value_store<VB, BF16>(vlo[k], vhi[k], q.j, D, q.vs, q.vz, q.vdst, doff, k * tpp * H * D * 2);
+    const uint32_t d = !LATE || k < valid ? doff : kOutside;
+    key_store<KB, ROT, STYLE, BF16>(klo[k], khi[k], q.kp, q.ks, q.kz, cs, q.kdst, d, k * tpp * H * D * 2);
+    value_store<VB, BF16>(vlo[k], vhi[k], q.j, D, q.vs, q.vz, q.vdst, d, k * tpp * H * D * 2);
   }
 }
 
-template <int TAG, bool ROT, int STYLE, bool BF16>
+template <int TAG, bool ROT, int STYLE, bool BF16, bool LATE>
 __device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u, const double* __restrict__ s_tab,
-                                             int t0, int head, int j) {
+                                             Stage& st, int t0, int head, int j) {
   Piece q;
   q.head = head;
   q.j = j;
   q.kp = key_piece<STYLE>(j, a.D, a.R);
   q.ks = q.kz = q.vs = q.vz = 0.f;
-  if constexpr (TAG != PKV_TAG_FP16) {
+  if constexpr (TAG != PKV_TAG_FP16 && !LATE) {
     const uint2 sw = *reinterpret_cast<const uint2*>(a.scales + u.scale_off + 4 * head);
     q.ks = half_bits_to_float(sw.x & 0xFFFFu);
     q.kz = half_bits_to_float(sw.x >> 16);
@@ -378,40 +436,77 @@ __device__ __forceinline__ void restore_unit(const KernelArgs& a, const Unit& u,
   }
   // A unit's rows share one page, carried in its work item.
   const int64_t page = int64_t(u.layer) * a.layer_elems + (int64_t(u.page1) << a.page_shift) * (int64_t(a.H) * a.D);
-  q.kdst = raw_rsrc(a.k_cache + page);
-  q.vdst = raw_rsrc(a.v_cache + page);
+  q.kdst = raw_rsrc(a.k_cache + page, LATE ? kOutside : kWholeRange);
+  q.vdst = raw_rsrc(a.v_cache + page, LATE ? kOutside : kWholeRange);
   q.doff = (uint32_t(u.row0 & ((int64_t(1) << a.log2P) - 1)) * uint32_t(a.H) + uint32_t(head)) * uint32_t(a.D) * 2;
   double2 cs[8];  // (cos, sin) of this thread's eight rotary pairs
-  if constexpr (ROT) {
+  if constexpr (ROT && !LATE) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) cs[e] = *reinterpret_cast<const double2*>(s_tab + 2 * (8 * j + e));
   }
   // A unit holds at most 4 * tpp tokens when H*D divides 4096, so a thread
   // has at most four; FP16 runs them two at a time (16-byte runs take twice
   // the registers).  Other shapes take the remaining tokens one by one.
-  const int nk = t0 < u.n_valid ? (u.n_valid - t0 + a.tpp - 1) / a.tpp : 0;
-  if constexpr (TAG != PKV_TAG_FP16) {
-    switch (nk) {
-      case 0: return;
-      case 1: restore_tokens<1, TAG, ROT, STYLE, BF16>(a, u, t0, q, cs); return;
-      case 2: restore_tokens<2, TAG, ROT, STYLE, BF16>(a, u, t0, q, cs); return;
-      case 3: restore_tokens<3, TAG, ROT, STYLE, BF16>(a, u, t0, q, cs); return;
-      case 4: restore_tokens<4, TAG, ROT, STYLE, BF16>(a, u, t0, q, cs); return;
-      default: break;
+  if constexpr (!LATE) {
+    const int nk = t0 < u.n_valid ? (u.n_valid - t0 + a.tpp - 1) / a.tpp : 0;
+    if constexpr (TAG != PKV_TAG_FP16) {
+      switch (nk) {
+        case 0: return;
+        case 1: restore_tokens<1, TAG, ROT, STYLE, BF16, false>(a, u, t0, q, cs, st, 1); return;
+        case 2: restore_tokens<2, TAG, ROT, STYLE, BF16, false>(a, u, t0, q, cs, st, 2); return;
+        case 3: restore_tokens<3, TAG, ROT, STYLE, BF16, false>(a, u, t0, q, cs, st, 3); return;
+        case 4: restore_tokens<4, TAG, ROT, STYLE, BF16, false>(a, u, t0, q, cs, st, 4); return;
+        default: break;
+      }
+    } else if (nk <= 4) {
+      for (int k = nk, t = t0; k > 0; k -= 2, t += 2 * a.tpp) {
+        if (k >= 2)
+          restore_tokens<2, TAG, ROT, STYLE, BF16, false>(a, u, t, q, cs, st, 2);
+        else
+          restore_tokens<1, TAG, ROT, STYLE, BF16, false>(a, u, t, q, cs, st, 1);
+      }
+      return;
     }
-  } else if (nk <= 4) {
-    for (int k = nk, t = t0; k > 0; k -= 2, t += 2 * a.tpp) {
-      if (k >= 2)
-        restore_tokens<2, TAG, ROT, STYLE, BF16>(a, u, t, q, cs);
-      else
-        restore_tokens<1, TAG, ROT, STYLE, BF16>(a, u, t, q, cs);
+    for (int t = t0; t < u.n_valid; t += a.tpp) restore_tokens<1, TAG, ROT, STYLE, BF16, false>(a, u, t, q, cs, st, 1);
+  } else {
+    // Late order: the switch takes lane 0's count, the largest in its wave
+    // (lanes are in token order; threads past tpp rows count 0), so each
+    // wave takes one case and passes the staging barrier once.
+    const int nk_t = t0 < a.tpp && t0 < u.n_valid ? (u.n_valid - t0 + a.tpp - 1) / a.tpp : 0;
+    const int nk = __builtin_amdgcn_readfirstlane(nk_t);
+    if constexpr (TAG != PKV_TAG_FP16) {
+      switch (nk) {
+        case 0: finish_stage<TAG, ROT>(st, q, cs); return;
+        case 1: restore_tokens<1, TAG, ROT, STYLE, BF16, true>(a, u, t0, q, cs, st, nk_t); return;
+        case 2: restore_tokens<2, TAG, ROT, STYLE, BF16, true>(a, u, t0, q, cs, st, nk_t); return;
+        case 3: restore_tokens<3, TAG, ROT, STYLE, BF16, true>(a, u, t0, q, cs, st, nk_t); return;
+        case 4: restore_tokens<4, TAG, ROT, STYLE, BF16, true>(a, u, t0, q, cs, st, nk_t); return;
+        default: break;
+      }
+    } else {
+      const int t2 = t0 + 2 * a.tpp;
+      switch (nk) {
+        case 0: finish_stage<TAG, ROT>(st, q, cs); return;
+        case 1: restore_tokens<1, TAG, ROT, STYLE, BF16, true>(a, u, t0, q, cs, st, nk_t); return;
+        case 2: restore_tokens<2, TAG, ROT, STYLE, BF16, true>(a, u, t0, q, cs, st, nk_t); return;
+        case 3:
+          restore_tokens<2, TAG, ROT, STYLE, BF16, true>(a, u, t0, q, cs, st, nk_t);
+          restore_tokens<1, TAG, ROT, STYLE, BF16, true>(a, u, t2, q, cs, st, nk_t - 2);
+          return;
+        case 4:
+          restore_tokens<2, TAG, ROT, STYLE, BF16, true>(a, u, t0, q, cs, st, nk_t);
+          restore_tokens<2, TAG, ROT, STYLE, BF16, true>(a, u, t2, q, cs, st, nk_t - 2);
+          return;
+        default: break;
+      }
     }
-    return;
+    finish_stage<TAG, ROT>(st, q, cs);
+    if (t0 < a.tpp)
+      for (int t = t0; t < u.n_valid; t += a.tpp) restore_tokens<1, TAG, ROT, STYLE, BF16, true>(a, u, t, q, cs, st, 1);
   }
-  for (int t = t0; t < u.n_valid; t += a.tpp) restore_tokens<1, TAG, ROT, STYLE, BF16>(a, u, t, q, cs);
 }
 
-template <bool BF16, int STYLE>
+template <bool BF16, int STYLE, bool LATE>
 __global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(KernelArgs a) {
   __shared__ __attribute__((aligned(16))) double s_tab[kMaxHeadDim];
   const Unit u = a.units[xcd_grouped(blockIdx.x, gridDim.x)];
@@ -419,27 +514,40 @@ __global__ __launch_bounds__(kWorkgroup, kMinWavesPerEU) void restore_kernel(Ker
   const int tid = threadIdx.x;
   const int tag = u.tag & 0xFF;
   const bool rot = (u.tag & kUnitRotate) != 0;
-  if (rot) {  // uniform across the workgroup
-    for (int i = tid; i < a.D; i += int(blockDim.x)) s_tab[i] = a.tables[u.table_off + i];
-    __syncthreads();
-  }
   // Thread -> (token, head, piece): shifts when the row's piece counts are
   // powers of two (uniform branches), divisions otherwise.
   const int t0 = a.cols_shift >= 0 ? tid >> a.cols_shift : tid / a.cols;
-  if (t0 >= a.tpp) return;
   const int c = tid - t0 * a.cols;
   const int dq = a.D >> 4;
   const int head = a.dq_shift >= 0 ? c >> a.dq_shift : c / dq;
   const int j = c - head * dq;
+  Stage st;
+  if constexpr (LATE) {
+    // Threads past tpp token rows have no tokens but take part in the barrier.
+    st.s_tab = s_tab;
+    st.table = a.tables + u.table_off;
+    st.tid = tid;
+    st.D = a.D;
+    st.threads = int(blockDim.x);
+    st.pending = true;
+    st.tval = rot && tid < a.D ? st.table[tid] : 0.0;
+    st.sw = tag != PKV_TAG_FP16 ? *reinterpret_cast<const uint2*>(a.scales + u.scale_off + 4 * head) : make_uint2(0, 0);
+  } else {
+    if (rot) {  // uniform across the workgroup
+      for (int i = tid; i < a.D; i += int(blockDim.x)) s_tab[i] = a.tables[u.table_off + i];
+      __syncthreads();
+    }
+    if (t0 >= a.tpp) return;
+  }
   switch (tag * 2 + (rot ? 1 : 0)) {
-    case 0: restore_unit<PKV_TAG_FP16, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
-    case 1: restore_unit<PKV_TAG_FP16, true, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
-    case 2: restore_unit<PKV_TAG_K8V8, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
-    case 3: restore_unit<PKV_TAG_K8V8, true, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
-    case 4: restore_unit<PKV_TAG_K8V4, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
-    case 5: restore_unit<PKV_TAG_K8V4, true, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
-    case 6: restore_unit<PKV_TAG_K4V4, false, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
-    default: restore_unit<PKV_TAG_K4V4, true, STYLE, BF16>(a, u, s_tab, t0, head, j); break;
+    case 0: restore_unit<PKV_TAG_FP16, false, STYLE, BF16, LATE>(a, u, s_tab, st, t0, head, j); break;
+    case 1: restore_unit<PKV_TAG_FP16, true, STYLE, BF16, LATE>(a, u, s_tab, st, t0, head, j); break;
+    case 2: restore_unit<PKV_TAG_K8V8, false, STYLE, BF16, LATE>(a, u, s_tab, st, t0, head, j); break;
+    case 3: restore_unit<PKV_TAG_K8V8, true, STYLE, BF16, LATE>(a, u, s_tab, st, t0, head, j); break;
+    case 4: restore_unit<PKV_TAG_K8V4, false, STYLE, BF16, LATE>(a, u, s_tab, st, t0, head, j); break;
+    case 5: restore_unit<PKV_TAG_K8V4, true, STYLE, BF16, LATE>(a, u, s_tab, st, t0, head, j); break;
+    case 6: restore_unit<PKV_TAG_K4V4, false, STYLE, BF16, LATE>(a, u, s_tab, st, t0, head, j); break;
+    default: restore_unit<PKV_TAG_K4V4, true, STYLE, BF16, LATE>(a, u, s_tab, st, t0, head, j); break;
   }
 }
 
@@ -486,6 +594,11 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   } else {
     (void)hipGetLastError();
   }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+    plan->restore_late_units = int64_t(cus) * restore_workgroups_per_cu(plan->host);
+  else
+    (void)hipGetLastError();
   if (total > 0) {
     hipError_t e = hipMalloc(&plan->device_mem, total);
     if (e != hipSuccess) {
@@ -571,6 +684,11 @@ pkv_status_t check_restore_buffers(const pkv_plan* plan, const void* payload, ui
   return PKV_OK;
 }
 
+// Start order of the restore kernel: 0 by launch size (late when every
+// workgroup of the launch fits on the device at once), 1 early, 2 late.
+// Set only through the test hook pkv_internal_set_restore_order.
+std::atomic<int> g_restore_order{0};
+
 // Enqueue the restore kernel over units [u0, u0 + n) of the plan, those whose
 // K rows start in payload bytes [win_lo, win_hi).
 pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const void* scales, void* k_cache,
@@ -603,14 +721,28 @@ pkv_status_t launch_restore(const pkv_plan* plan, const void* payload, const voi
   a.R = m.rotary_dim ? m.rotary_dim : m.head_dim;
   const dim3 grid(static_cast<uint32_t>(n)), block(plan->host.workgroup);
   const bool bf16 = m.out_dtype == PKV_OUT_BF16, half = m.rope_style == PKV_ROPE_HALF;
-  if (bf16 && half)
-    hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_HALF>), grid, block, plan->restore_lds, stream, a);
-  else if (bf16)
-    hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_INTERLEAVED>), grid, block, plan->restore_lds, stream, a);
-  else if (half)
-    hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_HALF>), grid, block, plan->restore_lds, stream, a);
-  else
-    hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_INTERLEAVED>), grid, block, plan->restore_lds, stream, a);
+  const int order = g_restore_order.load(std::memory_order_relaxed);
+  const bool late = order == 2 || (order == 0 && n <= plan->restore_late_units);
+  const uint32_t lds = plan->restore_lds;
+  if (late) {
+    if (bf16 && half)
+      hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_HALF, true>), grid, block, lds, stream, a);
+    else if (bf16)
+      hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_INTERLEAVED, true>), grid, block, lds, stream, a);
+    else if (half)
+      hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_HALF, true>), grid, block, lds, stream, a);
+    else
+      hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_INTERLEAVED, true>), grid, block, lds, stream, a);
+  } else {
+    if (bf16 && half)
+      hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_HALF, false>), grid, block, lds, stream, a);
+    else if (bf16)
+      hipLaunchKernelGGL((restore_kernel<true, PKV_ROPE_INTERLEAVED, false>), grid, block, lds, stream, a);
+    else if (half)
+      hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_HALF, false>), grid, block, lds, stream, a);
+    else
+      hipLaunchKernelGGL((restore_kernel<false, PKV_ROPE_INTERLEAVED, false>), grid, block, lds, stream, a);
+  }
   return hipGetLastError() == hipSuccess ? PKV_OK : PKV_ERR_DEVICE;
 }
 
@@ -661,6 +793,15 @@ bool pinned_host(const void* p) {
 }  // namespace pkv
 
 extern "C" {
+
+// Internal test hook (not part of pkv.h): force the restore kernel's start
+// order for every later launch in the process (0: by launch size, 1: early,
+// 2: late), so that tests cover both orders on every shape.
+pkv_status_t pkv_internal_set_restore_order(int32_t order) {
+  if (order < 0 || order > 2) return PKV_ERR_INVALID_ARGUMENT;
+  pkv::g_restore_order.store(order, std::memory_order_relaxed);
+  return PKV_OK;
+}
 
 pkv_status_t pkv_restore_plan(const pkv_model_t* model, const pkv_request_t* requests, int32_t num_requests,
                               pkv_plan_t** out) {

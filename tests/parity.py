@@ -10,6 +10,8 @@ element of both caches bit-identical to the pre-fill.
 """
 from __future__ import annotations
 
+import contextlib
+import ctypes
 import dataclasses
 import sys
 
@@ -173,7 +175,27 @@ def oracle_layer_checkpoint(case, ri: int, layer: int):
     return oq.quantize_rows(case.shape, case.requests[ri], kb, vb)
 
 
-def restore_small(case, poison: bool = True):
+# Start orders of the restore kernel (pkv_internal_set_restore_order): by
+# launch size, or forced to the early or the late order.
+ORDERS = {"auto": 0, "early": 1, "late": 2}
+
+
+@contextlib.contextmanager
+def restore_order(order: str):
+    """Force the restore kernel's start order for the launches inside."""
+    from paper_2609_26219_amd import binding as pb
+
+    fn = pb.load().pkv_internal_set_restore_order
+    fn.argtypes = [ctypes.c_int32]
+    fn.restype = ctypes.c_int32
+    assert fn(ORDERS[order]) == 0
+    try:
+        yield
+    finally:
+        assert fn(0) == 0
+
+
+def restore_small(case, poison: bool = True, order: str = "auto"):
     """Restore a small case on the GPU from the oracle's checkpoint.
     Returns (DeviceRestore after one run, (payload, scales) on the host)."""
     import torch
@@ -182,9 +204,17 @@ def restore_small(case, poison: bool = True):
 
     ckpt = oracle_checkpoint(case, poison)
     dr = DeviceRestore(case, checkpoint=ckpt)
-    dr.run()
-    torch.cuda.synchronize()
+    with restore_order(order):
+        dr.run()
+        torch.cuda.synchronize()
     return dr, ckpt
+
+
+def check_both_orders(case, poison: bool = True) -> None:
+    """Full-cache parity of the restore in the early and the late start order."""
+    for order in ("early", "late"):
+        st = check_full(*restore_small(case, poison, order))
+        log(f"  {order} order: {st}")
 
 
 # ---------------------------------------------------------------------------

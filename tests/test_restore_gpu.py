@@ -9,8 +9,8 @@ import oracle
 from paper_2609_26219_amd import binding as pb
 from paper_2609_26219_amd import workloads as wl
 
-from parity import (check_device_checkpoint, check_full, check_sampled, log, oracle_checkpoint,
-                    oracle_layer_checkpoint, poison_device, restore_small)
+from parity import (check_both_orders, check_device_checkpoint, check_full, check_sampled, log, oracle_checkpoint,
+                    oracle_layer_checkpoint, poison_device, restore_order, restore_small)
 
 pytestmark = pytest.mark.gpu
 
@@ -24,10 +24,11 @@ def torch():
     return _t
 
 
+@pytest.mark.parametrize("order", ["early", "late"])
 @pytest.mark.parametrize("name", ["tiny", "llama8b_1l"])
-def test_named_small_full(name, torch):
-    log(f"[gpu] {name}: full-cache parity")
-    dr, ckpt = restore_small(wl.make_case(name))
+def test_named_small_full(name, order, torch):
+    log(f"[gpu] {name}, {order} order: full-cache parity")
+    dr, ckpt = restore_small(wl.make_case(name), order=order)
     st = check_full(dr, ckpt)
     log(f"  {st}")
     assert st.bit_exact_fraction > 0.9999
@@ -39,10 +40,11 @@ def _paired(case):
     return case
 
 
+@pytest.mark.parametrize("order", ["early", "late"])
 @pytest.mark.parametrize("name", ["tiny", "llama8b_1l"])
-def test_named_small_full_paired_pages(name, torch):
-    log(f"[gpu] {name}, paired K/V pages: full-cache parity")
-    dr, ckpt = restore_small(_paired(wl.make_case(name)))
+def test_named_small_full_paired_pages(name, order, torch):
+    log(f"[gpu] {name}, paired K/V pages, {order} order: full-cache parity")
+    dr, ckpt = restore_small(_paired(wl.make_case(name)), order=order)
     st = check_full(dr, ckpt)
     log(f"  {st}")
     assert st.bit_exact_fraction > 0.9999
@@ -77,7 +79,7 @@ def test_paired_pages_argument_errors(torch):
 
 
 def test_tiny_k4v4_reading(torch):
-    check_full(*restore_small(wl.make_case("tiny", int4_tag=wl.TAG_K4V4)))
+    check_both_orders(wl.make_case("tiny", int4_tag=wl.TAG_K4V4))
 
 
 PROPERTY_CASES = [
@@ -105,7 +107,7 @@ def test_property_cases(params, layout, torch):
     if layout == wl.KV_PAIRED:
         _paired(case)
     log(f"[gpu] property case {params} layout {layout}")
-    check_full(*restore_small(case))
+    check_both_orders(case)
 
 
 @pytest.mark.parametrize("name", ["qwen3_32b_1l", "glm4_9b_1l", "llama33_70b_1l"])
@@ -114,9 +116,10 @@ def test_model_family_rope(name, torch):
     theta 1e6), GLM-4 (interleaved pairs on half the head), Llama-3.3
     (rotate-half with scaled frequencies)."""
     log(f"[gpu] {name}: full-cache parity with the model's RoPE")
-    st = check_full(*restore_small(wl.make_case(name)))
-    log(f"  {st}")
-    assert st.bit_exact_fraction > 0.9999
+    for order in ("early", "late"):
+        st = check_full(*restore_small(wl.make_case(name), order=order))
+        log(f"  {order} order: {st}")
+        assert st.bit_exact_fraction > 0.9999
 
 
 ROPE_CASES = [
@@ -139,7 +142,7 @@ def test_rope_variant_cases(params, torch):
     case.shape = dataclasses.replace(case.shape, rope_style=style, rotary_dim=0 if R == D else R,
                                      inv_freq=wl.llama3_inv_freq(5e5, R) if scaled else None)
     log(f"[gpu] rope variant {params}")
-    check_full(*restore_small(case))
+    check_both_orders(case)
 
 
 def test_all_repair_writes_nothing(torch):
@@ -153,8 +156,9 @@ def test_all_repair_writes_nothing(torch):
 def test_fp16_tag_zero_shift_is_bit_copy(torch):
     case = wl.make_custom(22, H=8, D=128, B=32, P=16, n_tokens=(300,), deltas=(0,), rho0s=(13,),
                           tag_set=(wl.TAG_FP16,), mix=(1.0,), repair_frac=0.1, out_dtype=wl.OUT_FP16)
-    st = check_full(*restore_small(case))
-    assert st.n_bit_exact == st.n
+    for order in ("early", "late"):
+        st = check_full(*restore_small(case, order=order))
+        assert st.n_bit_exact == st.n
 
 
 def test_restore_is_repeatable_and_plan_reusable(torch):
@@ -225,20 +229,29 @@ def test_streams(torch):
 # restore of the oracle's checkpoint on those pairs.
 # ---------------------------------------------------------------------------
 
-def _full_size(case, samples, torch):
+def _full_size(case, samples, torch, order="auto"):
     from paper_2609_26219_amd.device import DeviceRestore
     dr = DeviceRestore(case)
     refs = {key: oracle_layer_checkpoint(case, *key) for key in samples}
     check_device_checkpoint(case, dr.payload, dr.scales, refs)
     poison_device(case, dr.payload, dr.scales)
-    dr.run()
-    torch.cuda.synchronize()
+    with restore_order(order):
+        dr.run()
+        torch.cuda.synchronize()
     return check_sampled(dr, refs)
 
 
 def test_llama8b_32l_full_size(torch):
     log("[gpu] llama8b_32l: full-size checkpoint + restore, 3 sampled layers + untouched check")
     st = _full_size(wl.make_case("llama8b_32l"), [(0, 0), (0, 17), (0, 31)], torch)
+    log(f"  {st}")
+
+
+def test_llama8b_32l_full_size_late_order(torch):
+    """The late start order (chosen by size for launches that fit on the
+    device at once) forced on the full 32-layer launch."""
+    log("[gpu] llama8b_32l, late order forced: full-size checkpoint + restore, 2 sampled layers + untouched check")
+    st = _full_size(_paired(wl.make_case("llama8b_32l")), [(0, 1), (0, 29)], torch, order="late")
     log(f"  {st}")
 
 

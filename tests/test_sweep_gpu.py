@@ -4,7 +4,7 @@ write against the oracle quantizer (bit for bit)."""
 import pytest
 
 from paper_2609_26219_amd import binding as pb
-from parity import check_checkpoint_write, check_full, log, restore_small
+from parity import check_both_orders, check_checkpoint_write, log
 from sweep import LIMIT_CASES, SWEEP_SIZE, describe, limit_case, sweep_case
 
 pytestmark = pytest.mark.gpu
@@ -23,8 +23,7 @@ def torch():
 def test_sweep_parity(i, torch):
     case = sweep_case(i)
     log(f"[gpu] sweep {i}: {describe(case)}")
-    st = check_full(*restore_small(case))
-    log(f"  restore {st}")
+    check_both_orders(case)
     check_checkpoint_write(case, torch)
 
 
@@ -32,6 +31,5 @@ def test_sweep_parity(i, torch):
 def test_limit_parity(name, torch):
     case = limit_case(name)
     log(f"[gpu] limits {name}: {describe(case)}")
-    st = check_full(*restore_small(case))
-    log(f"  restore {st}")
+    check_both_orders(case)
     check_checkpoint_write(case, torch)

@@ -198,9 +198,9 @@ struct pkv_plan {
   // Dynamic LDS bytes per restore workgroup, sized so that at most
   // restore_workgroups_per_cu() workgroups are resident on a compute unit.
   uint32_t restore_lds = 0;
-  // Restore launches of at most this many units fit on the device at once
-  // (compute units x restore_workgroups_per_cu()) and take the late start
-  // order of the restore kernel; 0 when the device could not be queried.
+  // Restore launches of at most this many units (a few rounds of compute
+  // units x restore_workgroups_per_cu() resident workgroups) take the late
+  // start order of the restore kernel; 0 when the device could not be queried.
   int64_t restore_late_units = 0;
   // Streamed restore: copy streams and events (hipStream_t / hipEvent_t),
   // created on first use.  events[0] marks the caller's stream at entry;

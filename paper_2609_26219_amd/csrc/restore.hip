@@ -56,6 +56,10 @@ namespace {
 // keeps two to four).
 constexpr int kMinWavesPerEU = 4;
 
+// Launches of at most this many rounds of resident workgroups take the late
+// start order of the restore kernel (see Stage).
+constexpr int64_t kLateRounds = 6;
+
 struct KernelArgs {
   const Unit* units;
   const double* tables;
@@ -594,9 +598,13 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   } else {
     (void)hipGetLastError();
   }
+  // Late start order up to kLateRounds rounds of resident workgroups: with
+  // 8B-shaped rows (690 units per layer of an 8K-token suffix, 512 resident)
+  // it measured faster up to 4 layers (5.4 rounds), warm and cold, and
+  // slower cold from 6 layers (8 rounds) on.
   int cus = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
-    plan->restore_late_units = int64_t(cus) * restore_workgroups_per_cu(plan->host);
+    plan->restore_late_units = kLateRounds * int64_t(cus) * restore_workgroups_per_cu(plan->host);
   else
     (void)hipGetLastError();
   if (total > 0) {
@@ -684,8 +692,8 @@ pkv_status_t check_restore_buffers(const pkv_plan* plan, const void* payload, ui
   return PKV_OK;
 }
 
-// Start order of the restore kernel: 0 by launch size (late when every
-// workgroup of the launch fits on the device at once), 1 early, 2 late.
+// Start order of the restore kernel: 0 by launch size (late for launches of
+// at most kLateRounds rounds of resident workgroups), 1 early, 2 late.
 // Set only through the test hook pkv_internal_set_restore_order.
 std::atomic<int> g_restore_order{0};
 

@@ -199,7 +199,8 @@ struct pkv_plan {
   // restore_workgroups_per_cu() workgroups are resident on a compute unit.
   uint32_t restore_lds = 0;
   // Restore launches of at most this many units (a few rounds of compute
-  // units x restore_workgroups_per_cu() resident workgroups) take the late
+  // units x restore_workgroups_per_cu() resident workgroups; every launch for
+  // rows narrow enough for workgroups under kWorkgroup threads) take the late
   // start order of the restore kernel; 0 when the device could not be queried.
   int64_t restore_late_units = 0;
   // Streamed restore: copy streams and events (hipStream_t / hipEvent_t),

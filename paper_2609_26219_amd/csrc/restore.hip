@@ -17,7 +17,8 @@
 // them; a workgroup has 64 to 256 threads, restore_workgroup())
 // and issue the loads of all their tokens before the first store; the
 // unit's one page comes with its work item, so no workgroup-wide staging or
-// barrier is needed except for the per-request cos/sin table.  An LDS claim caps
+// barrier is needed except for the per-request cos/sin table (staged before
+// the payload loads or after them: the two start orders of Stage).  An LDS claim caps
 // the workgroups sharing a compute unit at two to four, chosen per plan from
 // its read:write byte ratio, its unit size, whether its keys rotate and the
 // cache layout (restore_workgroups_per_cu).
@@ -27,14 +28,15 @@
 // Both are addressed as page << page_shift slot rows from the layer's start.
 //
 // Arithmetic.  Codes decode exactly.  Keys are rotated in double precision
-// (v_fma_f64 issues at the rate of v_fma_f32 on CDNA4; an f32 rotation
-// measured no faster) with a double (cos, sin) table, so the rotated value
+// (v_fma_f64 issues at the rate of a non-packed v_fma_f32 on CDNA4, and
+// packed f32 is off in this build; an f32 rotation measured no faster) with
+// a double (cos, sin) table, so the rotated value
 // carries ~2^-53 relative error even under cancellation; values use one
 // single-precision FMA.  Results go to float, then to the cache dtype with
 // the hardware round-to-nearest-even conversions.
 //
 // Memory behaviour (8B-shaped 32K-token workload, measured): the kernel
-// moves 1.004x the algorithmic bytes; the write-heavy mixed stream bounds it,
+// moves 1.0025x the algorithmic bytes; the write-heavy mixed stream bounds it,
 // and paired pages let the memory system stream the writes faster.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -601,9 +603,15 @@ pkv_status_t upload_plan(HostPlan&& hp, pkv_plan** out) {
   // Late start order up to kLateRounds rounds of resident workgroups: with
   // 8B-shaped rows (690 units per layer of an 8K-token suffix, 512 resident)
   // it measured faster up to 4 layers (5.4 rounds), warm and cold, and
-  // slower cold from 6 layers (8 rounds) on.
+  // slower cold from 6 layers (8 rounds) on.  Rows narrow enough for
+  // workgroups under kWorkgroup threads take it at any depth: on the 32-layer
+  // 8B-shaped workload's share of one KV head per GPU (one-wave workgroups of
+  // two tokens per thread) it measured 102-112 us against 127-135 us, and
+  // within 1% of the early order at two and four heads.
   int cus = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+  if (plan->host.workgroup < kWorkgroup)
+    plan->restore_late_units = INT64_MAX;
+  else if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
     plan->restore_late_units = kLateRounds * int64_t(cus) * restore_workgroups_per_cu(plan->host);
   else
     (void)hipGetLastError();
@@ -692,8 +700,9 @@ pkv_status_t check_restore_buffers(const pkv_plan* plan, const void* payload, ui
   return PKV_OK;
 }
 
-// Start order of the restore kernel: 0 by launch size (late for launches of
-// at most kLateRounds rounds of resident workgroups), 1 early, 2 late.
+// Start order of the restore kernel: 0 by plan and launch size (late for
+// narrow rows and for launches of at most kLateRounds rounds of resident
+// workgroups), 1 early, 2 late.
 // Set only through the test hook pkv_internal_set_restore_order.
 std::atomic<int> g_restore_order{0};
 

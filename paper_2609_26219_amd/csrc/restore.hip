@@ -340,15 +340,16 @@ struct Piece {
   uint32_t doff;                      // bytes from the page's start to the thread's first token, its head
 };
 
-// Two orders of a workgroup's start.
+// Two orders of a workgroup's start, chosen per launch (launch_restore).
 //
-// Early (launches larger than the chip holds at once): the request's (cos,
-// sin) table is staged in LDS behind a barrier at the start, then each
-// thread loads its head's scales, then issues its payload loads.  Other
-// resident workgroups hide that chain of dependent loads.
+// Early (deep launches of 256-thread workgroups): the request's (cos, sin)
+// table is staged in LDS behind a barrier at the start, then each thread
+// loads its head's scales, then issues its payload loads.  Other resident
+// workgroups hide that chain of dependent loads.
 //
-// Late (launches whose workgroups are all resident at once, where nothing
-// hides it): table entry tid and the head's scale word are loaded at the
+// Late (launches a few rounds of resident workgroups deep, and narrow rows,
+// where too little other work hides it): table entry tid and the head's
+// scale word are loaded at the
 // start, the payload loads are issued right after, and only then are the
 // table entries written to LDS, the barrier passed and the scales
 // converted.  The table, the scales and the payload are then in flight

@@ -9,8 +9,9 @@
 // min/max is a wave reduction: no LDS and no barrier.  A lane holds its rows
 // in NL 16-byte registers between the range pass and the encode pass.
 //
-// Two kernels.  The tile kernel (blocks whose tile fits NL <= 8 loads per lane
-// and spans at most three cache pages, layer slices below 4 GiB) takes the
+// Three kernels.  The tile kernel (blocks whose tile fits NL <= 8 loads per
+// lane and spans at most three cache pages, layer slices below 4 GiB; tiles
+// of 9 to 16 loads go to its two-waves-per-tile form) takes the
 // block's source pages from its work item, so no page-table load sits in
 // front of the row loads; it uses 32-bit buffer offsets, consumes every
 // loaded register on every path, and issues every store (lanes with nothing
@@ -539,16 +540,8 @@ __device__ __forceinline__ void tile_store(const GatherArgs& a, const TileHdr& h
   }
 }
 
-// 16-load tiles (64-token blocks at head_dim 128) hold 64 registers of rows
-// per lane; with at most 8 waves per workgroup they get the 150 registers
-// they need without spilling (one workgroup per CU), measured 7% faster than
-// the same kernel squeezed into 128 registers for 16-wave workgroups (41
-// spilled) and 37% faster than the general kernel on the 70B-shaped write.
-constexpr int kTile16Threads = 512;
-
 template <bool BF16, int NL, bool STAGE>
-__global__ __launch_bounds__(NL == 16 ? kTile16Threads : kGatherMaxWaves * 64) void gather_tile_kernel(TileArgs s,
-                                                                             const Unit* __restrict__ units) {
+__global__ __launch_bounds__(kGatherMaxWaves * 64) void gather_tile_kernel(TileArgs s, const Unit* __restrict__ units) {
   extern __shared__ __attribute__((aligned(16))) uint8_t tile_image[];
   const GatherArgs& a = s.g;
   const int lane = threadIdx.x & 63;
@@ -564,6 +557,122 @@ __global__ __launch_bounds__(NL == 16 ? kTile16Threads : kGatherMaxWaves * 64) v
   load_tile<NL>(a, h, r, c, w);
   const Quant q = tile_range<BF16, NL>(a, h, r, w, sb, zb);
   tile_store<BF16, NL, STAGE>(a, h, r, c, on, w, q, sb, zb, tile_image);
+}
+
+// Tiles of 9 to 16 loads per lane (64-token blocks at head_dim 128) as two
+// halves on two waves: each wave holds 8 loads (rows [32h, 32h + 32) at
+// head_dim 128), the pair exchanges its tile's range through LDS behind the
+// workgroup's one barrier, then each wave encodes and stores its half.  An
+// 8-wave workgroup holds the two halves of four consecutive tiles.  Held
+// whole by one wave, such a tile needs 150 registers and a workgroup per CU;
+// as halves it takes 76 (three workgroups per CU), measured 6.6% faster on the
+// 70B-shaped write (5488-5494 against 5880-5889 us).  Every wave passes the
+// barrier exactly once, FP16 tiles and waves past the last tile included.
+constexpr int kHalfWaves = 8;
+
+template <bool BF16>
+__global__ __launch_bounds__(kHalfWaves * 64) void gather_half_kernel(TileArgs s, const Unit* __restrict__ units) {
+  __shared__ float s_rng[kHalfWaves][2];
+  const GatherArgs& a = s.g;
+  constexpr int NL = 8;
+  const int lane = threadIdx.x & 63;
+  const int r = lane / a.lpr;
+  const int c = lane - r * a.lpr;
+  const bool on = r < a.rpl;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t W = xcd_grouped(blockIdx.x, gridDim.x) * kHalfWaves + wave;
+  const int64_t T = W >> 1;
+  const int half = int(W & 1);
+  const bool live = T < s.num_tiles;  // uniform per wave; every wave still passes the barrier
+  const TileHdr h = tile_header(a, units, live ? T : 0);
+  const int t_base = half * NL * a.rpl;
+  uint4 w[NL];
+  {
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(h.src), 0, h.range, 0x00020000);
+    const uint32_t row_bytes = uint32_t(a.H) * uint32_t(a.D) * 2u;
+    const uint32_t slot_mask = (1u << a.log2P) - 1;
+    const uint32_t slot0 = uint32_t(h.row0) & slot_mask;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int t = t_base + i * a.rpl + r;
+      const uint32_t pos = slot0 + uint32_t(t < h.n_valid ? t : 0);
+      const uint32_t k = pos >> a.log2P;
+      const uint32_t page = uint32_t(h.page0) + (k >= 1 ? uint32_t(h.page1 - h.page0) : 0u) +
+                            (k >= 2 ? uint32_t(h.page2 - h.page1) : 0u);
+      const uint32_t off = ((page << a.page_shift) | (pos & slot_mask)) * row_bytes + 16u * uint32_t(c);
+      w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kNonTemporal));
+    }
+  }
+  const uint32_t H = uint32_t(a.H), D = uint32_t(a.D);
+  const bool lane0 = lane == 0;
+  const __amdgpu_buffer_rsrc_t out = __builtin_amdgcn_make_buffer_rsrc(h.tile, 0, live ? h.tile_bytes : 0u, 0x00020000);
+  if (h.bits == 16) {
+    __syncthreads();  // matches the range exchange of the other tags (uniform per workgroup)
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int t = t_base + i * a.rpl + r;
+      const uint4 v = t < h.n_valid ? to_half8<BF16>(w[i]) : make_uint4(0, 0, 0, 0);
+      const uint32_t off = on && t < a.B ? (uint32_t(t) * H + uint32_t(h.head)) * D * 2 + 16u * uint32_t(c) : kDropOffset;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), out, off, 0, kNonTemporal);
+    }
+    if (lane0 && half == 0 && live) *h.scale_word = 0u;
+    return;
+  }
+  float mn = __builtin_inff(), mx = -__builtin_inff();
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const uint32_t word = word_of(w[i], 2 * p);
+      const float x0 = cache_value<BF16>(word, 0);
+      const float x1 = BF16 ? __uint_as_float(word) : cache_value<BF16>(word, 1);
+      mn = __builtin_fminf(__builtin_fminf(mn, x0), x1);
+      mx = __builtin_fmaxf(__builtin_fmaxf(mx, x0), x1);
+    }
+  }
+  wave_range(mn, mx);
+  if (lane0) {
+    s_rng[wave][0] = mn;
+    s_rng[wave][1] = mx;
+  }
+  __syncthreads();
+  mn = __builtin_fminf(mn, s_rng[wave ^ 1][0]);
+  mx = __builtin_fmaxf(mx, s_rng[wave ^ 1][1]);
+  if (BF16) {
+    mn = __uint_as_float(__float_as_uint(mn) & 0xFFFF0000u);
+    mx = __uint_as_float(__float_as_uint(mx) & 0xFFFF0000u);
+  }
+  Quant q;
+  const double qmax = double((1 << h.bits) - 1);
+  const uint16_t zb = f16_floor(static_cast<double>(mn) + 0.0);
+  q.zero = f16_value(zb);
+  const uint16_t sb = f16_ceil(((static_cast<double>(mx) - q.zero) + 0.0) / qmax);
+  q.scale = f16_value(sb);
+  q.zf = static_cast<float>(q.zero);
+  q.invf = q.scale != 0.0 ? static_cast<float>(1.0 / q.scale) : 0.0f;
+  q.qmax = uint32_t((1 << h.bits) - 1);
+  const bool flat = q.scale == 0.0;
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int t = t_base + i * a.rpl + r;
+    const bool valid = t < h.n_valid && !flat;
+    const bool store = on && t < a.B;
+    const uint4 x = fresh(w[i]);
+    if (h.bits == 8) {
+      uint2 v = make_uint2(encode_word<BF16, 4>(make_uint4(x.x, x.y, 0, 0), q),
+                           encode_word<BF16, 4>(make_uint4(x.z, x.w, 0, 0), q));
+      v = valid ? v : make_uint2(0, 0);
+      const uint32_t at = (uint32_t(t) * H + uint32_t(h.head)) * D + 8u * uint32_t(c);
+      __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), out, store ? at : kDropOffset, 0, kNonTemporal);
+    } else {
+      uint32_t v = encode_word<BF16, 8>(x, q);
+      v = valid ? v : 0u;
+      const uint32_t at = (uint32_t(t) * H + uint32_t(h.head)) * (D / 2) + 4u * uint32_t(c);
+      __builtin_amdgcn_raw_buffer_store_b32(v, out, store ? at : kDropOffset, 0, kNonTemporal);
+    }
+  }
+  if (lane0 && half == 0 && live) *h.scale_word = uint32_t(sb) | (uint32_t(zb) << 16);
 }
 
 // The staged store needs a workgroup to hold exactly the heads of one
@@ -587,7 +696,11 @@ hipError_t launch_tile(const TileArgs& s, const Unit* units, int nl, int wg, uin
     case 2: return launch_tile_nl<BF16, 2>(s, units, wg, image, stream);
     case 4: return launch_tile_nl<BF16, 4>(s, units, wg, image, stream);
     case 8: return launch_tile_nl<BF16, 8>(s, units, wg, image, stream);
-    default: return launch_tile_nl<BF16, 16>(s, units, wg, image, stream);
+    default: {
+      const dim3 grid(static_cast<uint32_t>((2 * s.num_tiles + kHalfWaves - 1) / kHalfWaves));
+      hipLaunchKernelGGL((gather_half_kernel<BF16>), grid, dim3(kHalfWaves * 64), 0, stream, s, units);
+      return hipGetLastError();
+    }
   }
 }
 
@@ -673,19 +786,17 @@ pkv_status_t pkv_quantize_gather(const pkv_plan_t* plan, const void* k_cache, co
   const int nl = pkv::gather_loads_per_chunk(nload);
   a.nchunk = (nload + nl - 1) / nl;
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  if (a.nchunk == 1 && (nl <= 8 || plan->host.workgroup <= pkv::kTile16Threads) &&
-      m.block_tokens <= 2 * m.page_size + 1 && a.layer_elems * 2 < (int64_t(1) << 32)) {
-    // Tiles of at most 8 loads per lane (16 with workgroups of at most 8
-    // waves) on at most kUnitPages pages, layer slices below 4 GiB: the tile
-    // kernel.
+  if (a.nchunk == 1 && m.block_tokens <= 2 * m.page_size + 1 && a.layer_elems * 2 < (int64_t(1) << 32)) {
+    // Tiles of at most 16 loads per lane on at most kUnitPages pages, layer
+    // slices below 4 GiB: the tile kernel (up to 8 loads) or the half-tile
+    // kernel (9 to 16).
     pkv::TileArgs sa;
     sa.g = a;
     sa.num_tiles = info.num_units * 2 * m.num_kv_heads;
     // Staged stores when a workgroup is one wave per head of one (block, K|V)
-    // and several workgroups share a compute unit: 16-load tiles run one
-    // workgroup per CU (150 registers), where the barrier would leave the CU
-    // without loads in flight while it writes (measured 20% slower on the
-    // 70B-shaped write).
+    // of at most 8 loads per lane.  (Larger tiles staged whole in a
+    // workgroup per CU ran 18-20% slower on the 70B-shaped write: the barrier
+    // left the CU without loads in flight while it wrote.)
     const uint64_t image = uint64_t(m.block_tokens) * m.num_kv_heads * m.head_dim;
     const uint32_t stage =
         nl <= 8 && plan->host.workgroup == 64 * m.num_kv_heads && image <= pkv::kTileImageMax ? uint32_t(image) : 0;

@@ -186,8 +186,7 @@ def test_gather_addresses_paired_pages(maker):
                            tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
 ], ids=["tiny", "h8_b4_two_requests", "h4_d64_b64", "h8_d128", "h20_heads_loop", "h8_d128_b64_p32"])
 def test_tile_kernel_tiles_and_pages(maker):
-    """Tile kernel (blocks of at most 2P + 1 tokens, at most 8 loads per lane,
-    16 with workgroups of at most 8 waves):
+    """Tile kernel (blocks of at most 2P + 1 tokens, at most 16 loads per lane):
     wave w of workgroup b encodes tile b * waves + w of the (unit, K|V, head)
     order, so a grid of ceil(tiles / waves) workgroups encodes every tile
     exactly once; the three source pages carried in each unit give every
@@ -210,7 +209,7 @@ def test_tile_kernel_tiles_and_pages(maker):
     lpr = D // 8
     rpl = 64 // lpr
     nload = -(-B // rpl)
-    assert loads_per_chunk(nload) <= (16 if WG <= 512 else 8) and loads_per_chunk(nload) >= nload
+    assert loads_per_chunk(nload) <= 16 and loads_per_chunk(nload) >= nload
     for u in units:
         pages = [int(u["table_off"]), int(u["page1"]), int(u["page2"])]  # page0 shares table_off's slot
         first = int(u["row0"]) // P
@@ -220,3 +219,49 @@ def test_tile_kernel_tiles_and_pages(maker):
             assert 0 <= k <= 2
             assert pages[k] == pt_all[int(u["pt_off"]) + row // P]
             assert 0 <= pages[k] < s.pool_pages
+
+
+HALF_WAVES = 8  # waves per workgroup of the half-tile kernel
+
+
+@pytest.mark.parametrize("maker", [
+    lambda: wl.make_custom(13, L=1, H=8, D=128, B=64, P=32, n_tokens=(150, 64), deltas=(4096, 0), rho0s=(31, 96),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+    # 12 loads per lane (a 16-load chunk), three heads: tiles of different (unit, K|V) share workgroups
+    lambda: wl.make_custom(14, L=2, H=3, D=128, B=48, P=32, n_tokens=(100,), deltas=(7,), rho0s=(5,),
+                           tag_set=(0, 1, 2, 3), mix=(1, 1, 1, 1)),
+], ids=["h8_d128_b64_p32", "h3_d128_b48"])
+def test_half_tile_kernel_mapping(maker):
+    """Half-tile kernel (9 to 16 loads per lane): wave w of workgroup b is
+    half-tile W = 8b + w, tile W >> 1, half W & 1, so both halves of a tile sit
+    in one workgroup (the range exchange), every tile is covered exactly once
+    by its two halves' rows, and each tile's scale word is written once."""
+    case = maker()
+    s = case.src_shape
+    H, D, B = s.num_kv_heads, s.head_dim, s.block_tokens
+    units, _ = checkpoint_units(s, case.requests)
+    lpr = D // 8
+    rpl = 64 // lpr
+    nload = -(-B // rpl)
+    assert 8 < nload <= 16 and loads_per_chunk(nload) == 16
+    ntiles = len(units) * 2 * H
+    grid = -(-2 * ntiles // HALF_WAVES)
+    lane = np.arange(64)
+    r, c = lane // lpr, lane % lpr
+    on = r < rpl
+    rows_of = np.zeros((ntiles, B, lpr), dtype=np.int32)  # (tile, row, channel piece) writes
+    scale_writes = np.zeros(ntiles, dtype=np.int32)
+    for b in range(grid):
+        for w in range(HALF_WAVES):
+            W = b * HALF_WAVES + w
+            T, half = W >> 1, W & 1
+            assert (W ^ 1) // HALF_WAVES == b  # the partner half is in the same workgroup
+            if T >= ntiles:
+                continue  # such waves read tile 0, store nothing, and still pass the barrier
+            for i in range(8):
+                t = half * 8 * rpl + i * rpl + r
+                st = on & (t < B)
+                np.add.at(rows_of[T], (t[st], c[st]), 1)
+            if half == 0:
+                scale_writes[T] += 1
+    assert (rows_of == 1).all() and (scale_writes == 1).all()

@@ -346,7 +346,8 @@ pkv_status_t pkv_plan_repair(int32_t suffix_tokens, int32_t block_tokens, int64_
  * suffix rows encoded per cache. */
 typedef struct {
   int64_t num_requests;
-  int64_t num_units;          /* (request, layer, reused block) work units = workgroups launched */
+  int64_t num_units;          /* work items: restore plans, the part of a reused block of one layer inside one
+                                 cache page (one workgroup each); checkpoint plans, (request, layer, block) */
   int64_t restored_rows;      /* token rows written per cache, summed over layers and requests */
   uint64_t payload_bytes;     /* bytes of `payload` the plan may touch (max over requests of offset + size) */
   uint64_t scale_bytes;       /* bytes of `scales` likewise */
